@@ -1,0 +1,177 @@
+"""Benchmark of the fused linear + cross-entropy forward + backward step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload llama3_8b] [--gpus 1]
+
+One step = one lce_forward_backward call (loss, dH, dW) over the whole synthetic batch, inputs
+already resident in HBM. Prints ONE JSON line with tokens/s, the fraction of the bf16 dense MFMA
+peak (credited work 6*N*H*V), the live roofline of the dominant kernel (HIP events recorded by the
+library on its launch stream), peak device memory against a materialised-logits PyTorch baseline,
+and the float64 CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+METRIC = "fused LCE fwd+bwd tokens/s and % bf16 MFMA peak (H=4096,V=128256,N=8192)"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(d, tokens: int):
+    """The float64 oracle, as it stands, on the first `tokens` tokens (all of V and H)."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # threadpoolctl missing: report the affinity mask
+        threads = len(os.sched_getaffinity(0))
+    n = min(tokens, d["N"])
+    X, y = d["hidden"][:n], d["labels"][:n]
+    t = time.perf_counter()
+    oracle.forward_backward(X, d["weight"], y, d["ignore_index"], d["reduction"], rows_per_block=256)
+    dt = time.perf_counter() - t
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} of {d['N']} tokens of {d['name']} (full V={d['V']}, H={d['H']}), float64 "
+                      f"forward+backward incl. upcast, {dt:.1f} s"}
+
+
+def materialised_baseline(X, W, y, ignore_index, reduction, reps=3):
+    """Peak memory and time of the plain PyTorch step that builds the N x V logits."""
+    import torch
+    import torch.nn.functional as F
+    Xg = X.detach().clone().requires_grad_(True)
+    Wg = W.detach().clone().requires_grad_(True)
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    times = []
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        logits = Xg @ Wg.T
+        loss = F.cross_entropy(logits.float(), y, ignore_index=ignore_index, reduction=reduction)
+        gx, gw = torch.autograd.grad(loss, [Xg, Wg])
+        e.record()
+        torch.cuda.synchronize()
+        times.append(s.elapsed_time(e))
+        del logits, loss, gx, gw
+    peak = torch.cuda.max_memory_allocated() - base
+    del Xg, Wg
+    torch.cuda.empty_cache()
+    return peak, min(times)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3_8b")
+    ap.add_argument("--chunk", type=int, default=0, help="tokens per chunk (0 = automatic)")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2603_16428_amd as lce
+    import workloads
+
+    lce.load_library()
+    t0 = time.time()
+    d = workloads.make_inputs(args.workload, seed=0)
+    N, H, V = d["N"], d["H"], d["V"]
+    log(f"inputs {args.workload} N={N} H={H} V={V} ready in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    X, W, y = d["hidden"].to(dev), d["weight"].to(dev), d["labels"].to(dev)
+    dtype = X.dtype
+    chunk = args.chunk or lce.auto_chunk_tokens(N, H, V, dtype)
+    chunks = -(-N // chunk)
+
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    ws = torch.empty(lce.workspace_size(N, H, V, dtype, True, args.chunk), dtype=torch.uint8, device=dev)
+    out = (torch.empty(1, dtype=torch.float32, device=dev), torch.empty_like(X), torch.empty_like(W))
+    lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
+    torch.cuda.synchronize()
+    lce_peak = torch.cuda.max_memory_allocated() - base
+
+    for _ in range(args.warmup):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps), loss {out[0].item():.6f}")
+
+    stream = torch.cuda.current_stream()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    lce.timing_enable(True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    kern = lce.timing_read()
+    lce.timing_enable(False)
+    ms = total_ms / args.steps
+    log(f"timed {args.steps} steps: {ms:.3f} ms/step; per kind: "
+        + ", ".join(f"{k} {v[0] / args.steps:.3f} ms ({v[1]} launches)" for k, v in kern.items()))
+
+    flops = 6.0 * N * H * V
+    peak = PEAK_BF16_TFLOPS if dtype == torch.bfloat16 else PEAK_FP32_TFLOPS
+    tflops = flops / (ms * 1e-3) / 1e12
+    # Dominant kernel: the GEMM kind with the largest share of the step. Each of the three
+    # contractions performs 2*N*H*V flops per step, spread over its launches.
+    gemm_kinds = ("logits_lse_gemm", "dh_gemm", "dw_gemm")
+    dom = max(gemm_kinds, key=lambda k: kern[k][0])
+    dom_ms, dom_launches = kern[dom]
+    per_launch_flops = 2.0 * N * H * V * args.steps / dom_launches
+    achieved = per_launch_flops / (dom_ms / dom_launches * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                "per_launch_flops": per_launch_flops, "avg_launch_ms": dom_ms / dom_launches,
+                "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()}}
+
+    memory = {"lce_peak_bytes": int(lce_peak)}
+    if not args.no_memory:
+        del ws
+        torch.cuda.empty_cache()
+        mpeak, mtime = materialised_baseline(X, W, y, d["ignore_index"], d["reduction"])
+        memory.update({"materialised_peak_bytes": int(mpeak), "reduction_vs_materialised": round(1 - lce_peak / mpeak, 4),
+                       "materialised_ms_per_step": round(mtime, 3)})
+        log(f"materialised baseline: peak {mpeak / 1e9:.2f} GB, {mtime:.2f} ms; LCE peak {lce_peak / 1e9:.2f} GB")
+
+    result = {
+        "metric": METRIC, "value": round(N / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if dtype == torch.bfloat16 else "f32",
+        "data": "synthetic", "tflops": round(tflops, 1), "mfma_peak_frac": round(tflops / peak, 4),
+        "config": {"workload": args.workload, "N": N, "H": H, "V": V, "reduction": d["reduction"],
+                   "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
+        "roofline": roofline, "memory": memory,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle on the host cores ...")
+        result["cpu_baseline"] = cpu_baseline(d, args.cpu_sample_tokens)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

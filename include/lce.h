@@ -1,0 +1,125 @@
+/*
+ * lce.h -- C ABI of the fused linear + cross-entropy (LCE) step for MI355X (gfx950).
+ *
+ * The operation is the output layer of a language model and its loss:
+ *
+ *     logits   z_i = W x_i                       (x_i = row i of hidden[N,H], W = weight[V,H])
+ *     lse_i    = log sum_v exp(z_iv)
+ *     l_i      = lse_i - z_{i,y_i}  for y_i != ignore_index, else 0
+ *     loss     = sum_i l_i / n_valid   (MEAN; n_valid = number of non-ignored tokens)
+ *              | sum_i l_i             (SUM)
+ *              | l                     (NONE, forward only)
+ *     dZ_i     = g_i (softmax(z_i) - onehot(y_i)),  g_i = [y_i != ignore_index] / n_valid (MEAN) or 1 (SUM)
+ *     dH = grad_hidden = dZ W,   dW = grad_weight = dZ^T X
+ *
+ * This is the paper's fused LinearCrossEntropy kernel (Section 3.3, "Integrated I/O and Compute
+ * Co-Design", paragraph "Optimized Triton Kernels"): the projection is fused with the loss and the
+ * gradients are produced chunk by chunk over the tokens, so that the N x V logits tensor is never
+ * held in memory. The mixed-precision convention (bf16 tensors on the GPU, fp32 where precision
+ * matters) follows Section 2.1 ("Static footprints") and Section 3.2.
+ *
+ * Conventions for every entry point
+ *   - All tensor pointers are DEVICE pointers owned by the caller, row-major and contiguous:
+ *     hidden [N,H], weight [V,H], labels [N] (int64), grad_hidden [N,H], grad_weight [V,H].
+ *     hidden, weight, grad_hidden and grad_weight have the element type `dtype`.
+ *     Pointers must be 16-byte aligned.
+ *   - The library never allocates, frees or synchronises. Scratch memory comes from the caller
+ *     (`workspace`, device memory of at least lce_workspace_size(...) bytes, 256-byte aligned).
+ *   - Work is enqueued in order on `stream` (a hipStream_t; NULL = the default stream) and the call
+ *     returns without waiting. Outputs are overwritten, never accumulated into.
+ *   - Arguments are validated before anything is enqueued; on any error nothing is launched.
+ *   - Results are deterministic: the same inputs on the same device give bitwise equal outputs
+ *     (no atomics; every reduction has a fixed order).
+ *   - Arithmetic: bf16 operands with fp32 accumulation (dtype BF16) or fp32 throughout (FP32).
+ *     loss and lse are fp32; grad_hidden and grad_weight have the input dtype.
+ *   - A non-ignored label outside [0, V) is not an error the call can report (labels live on the
+ *     device); its token's loss becomes NaN and it contributes no one-hot term to the gradients.
+ *   - MEAN with no valid token gives loss 0 and zero gradients.
+ *   - Supported shapes: N, H, V >= 1; H a multiple of 8 (BF16) or 4 (FP32); V * H and N * H
+ *     below 2^31 elements per 256-row slice limits (see LCE_ERR_UNSUPPORTED).
+ */
+#ifndef LCE_H_
+#define LCE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LCE_OK = 0,
+  LCE_ERR_INVALID_ARGUMENT = 1,    /* null pointer, size < 1, unknown enum, NONE with backward */
+  LCE_ERR_UNSUPPORTED = 2,         /* valid but outside the supported shapes (see above)      */
+  LCE_ERR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes < lce_workspace_size(...)               */
+  LCE_ERR_HIP = 4                  /* the HIP runtime reported an error while enqueueing      */
+} lce_status_t;
+
+typedef enum { LCE_DTYPE_FP32 = 0, LCE_DTYPE_BF16 = 1 } lce_dtype_t;
+
+/* Same order as torch's reduction enum. */
+typedef enum { LCE_REDUCTION_NONE = 0, LCE_REDUCTION_MEAN = 1, LCE_REDUCTION_SUM = 2 } lce_reduction_t;
+
+/*
+ * Bytes of device workspace needed by lce_forward (with_backward = 0) or lce_forward_backward
+ * (with_backward = 1) for these sizes. chunk_tokens is the number of tokens processed per chunk
+ * (0 = automatic: the largest multiple of 64 not above min(H, ceil(N/2)), at least 64; a nonzero
+ * value smaller than N must be a multiple of 64). The workspace holds O(chunk_tokens * V + V * H)
+ * elements; the N x V logits never exist. Returns 0 for invalid arguments.
+ */
+size_t lce_workspace_size(int64_t N, int64_t H, int64_t V, int dtype, int with_backward,
+                          int64_t chunk_tokens);
+
+/* The chunk size lce_forward_backward uses for chunk_tokens = 0 (automatic), or 0 if invalid. */
+int64_t lce_auto_chunk_tokens(int64_t N, int64_t H, int64_t V, int dtype);
+
+/*
+ * Forward only: the loss, and optionally each token's log-sum-exp.
+ *   loss : device fp32, [1] for MEAN/SUM, [N] for NONE (per-token losses, 0 for ignored tokens).
+ *   lse  : device fp32 [N], or NULL. Filled for every token, ignored ones included.
+ * Performs 2*N*H*V flops of contraction.
+ */
+lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* labels,
+                         int64_t N, int64_t H, int64_t V, int dtype,
+                         int64_t ignore_index, int reduction,
+                         float* loss, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Forward and backward: the reduced loss and its gradients with respect to hidden and weight
+ * (upstream gradient 1; scale both outputs for another upstream value).
+ *   reduction   : MEAN or SUM (NONE returns LCE_ERR_INVALID_ARGUMENT).
+ *   loss        : device fp32 [1].
+ *   grad_hidden : device [N,H] of dtype; grad_weight: device [V,H] of dtype.
+ *   chunk_tokens: as for lce_workspace_size (pass the same value).
+ * Performs 6*N*H*V flops of contraction.
+ */
+lce_status_t lce_forward_backward(const void* hidden, const void* weight, const int64_t* labels,
+                                  int64_t N, int64_t H, int64_t V, int dtype,
+                                  int64_t ignore_index, int reduction,
+                                  float* loss, void* grad_hidden, void* grad_weight,
+                                  int64_t chunk_tokens,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Per-kernel timing, for measurement tools (not for concurrent use). While enabled, every launch of
+ * lce_forward / lce_forward_backward is bracketed by two hipEvents recorded on the call's stream.
+ * lce_timing_read waits for the recorded events and returns, per kernel kind, the total elapsed
+ * milliseconds and the number of launches since the last enable; the events are then released.
+ * Kinds: 0 logits GEMM + log-sum-exp, 1 dH GEMM (with its split reduction), 2 dW GEMM,
+ * 3 dlogits, 4 transposes of W and X, 5 the remaining small kernels.
+ * lce_timing_enable(1) resets the totals; (0) stops recording. Returns LCE_OK or LCE_ERR_HIP.
+ */
+#define LCE_TIMING_KINDS 6
+lce_status_t lce_timing_enable(int enable);
+lce_status_t lce_timing_read(double* ms, int64_t* launches, int n_kinds);
+
+/* A static, human-readable name for a status code. */
+const char* lce_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LCE_H_ */

@@ -1,0 +1,415 @@
+// C ABI of the fused linear + cross-entropy step: argument checks, workspace plan, chunk loop.
+//
+// Per call (Section 3.3, "Optimized Triton Kernels": projection fused with the loss, gradients in
+// token chunks, the N x V logits never held):
+//   count valid labels (global mean divisor) -> target logits -> [backward: W^T, X^T]
+//   for each chunk of n_c tokens:
+//     logits^T tile GEMM with the log-sum-exp epilogue  (stores e = exp(z - m_slice) for backward)
+//     row combine -> lse, token losses
+//     [backward] dlogits (in place, plus its transpose) -> dH rows GEMM -> dW GEMM (fp32 accumulate
+//                across chunks in a fixed order; the last chunk writes the output dtype)
+//   loss reduction (fp64, fixed order)
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "lce.h"
+#include "lce_aux.hpp"
+#include "lce_gemm.hpp"
+
+namespace lce {
+namespace {
+
+constexpr int64_t kAlign = 256;
+constexpr int kMaxDevices = 64;
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// ---- optional per-kernel timing (events on the launch stream) ----
+enum TimingKind { T_LOGITS = 0, T_DH = 1, T_DW = 2, T_DLOGITS = 3, T_TRANSPOSE = 4, T_OTHER = 5, T_KINDS = 6 };
+struct TimedLaunch {
+  int kind;
+  hipEvent_t start, stop;
+};
+std::mutex g_timing_mu;
+bool g_timing_on = false;
+std::vector<TimedLaunch> g_timed;
+
+// Brackets the launches made during its lifetime with events when timing is enabled.
+class KernelTimer {
+ public:
+  KernelTimer(int kind, hipStream_t s) : kind_(kind), s_(s) {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    if (!g_timing_on) return;
+    if (hipEventCreate(&start_) != hipSuccess) return;
+    if (hipEventCreate(&stop_) != hipSuccess) { (void)hipEventDestroy(start_); return; }
+    active_ = hipEventRecord(start_, s_) == hipSuccess;
+  }
+  ~KernelTimer() {
+    if (!active_) return;
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    if (hipEventRecord(stop_, s_) == hipSuccess) {
+      g_timed.push_back({kind_, start_, stop_});
+    } else {
+      (void)hipEventDestroy(start_);
+      (void)hipEventDestroy(stop_);
+    }
+  }
+
+ private:
+  int kind_;
+  hipStream_t s_;
+  hipEvent_t start_ = nullptr, stop_ = nullptr;
+  bool active_ = false;
+};
+int64_t cdiv(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+struct Plan {
+  int64_t N = 0, H = 0, V = 0;
+  int esz = 0;
+  bool backward = false;
+  int64_t nc = 0, chunks = 0;     // tokens per chunk, number of chunks
+  int64_t Vp = 0, ncp = 0, Np = 0;
+  int64_t slices = 0;
+  int dh_splits = 1;
+  int64_t dh_kps = 0;             // K (vocabulary) per dH split, multiple of the K-tile
+  // workspace offsets (bytes)
+  size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_zt = 0,
+         o_wt = 0, o_xt = 0, o_acc = 0, o_dhp = 0;
+  size_t total = 0;
+};
+
+int num_cus() {
+  static std::atomic<int> cached{0};
+  int c = cached.load();
+  if (c > 0) return c;
+  int dev = 0;
+  hipDeviceProp_t p;
+  if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&p, dev) == hipSuccess &&
+      p.multiProcessorCount > 0) {
+    c = p.multiProcessorCount;
+  } else {
+    c = 256;
+  }
+  cached.store(c);
+  return c;
+}
+
+int64_t auto_chunk(int64_t N, int64_t H) {
+  const int64_t half = cdiv(N, 2);
+  int64_t nc = std::min(H, half) / 64 * 64;
+  return std::max<int64_t>(64, nc);
+}
+
+bool dtype_ok(int dtype) { return dtype == LCE_DTYPE_FP32 || dtype == LCE_DTYPE_BF16; }
+
+// Fills `p`; returns LCE_OK or the status that the sizes deserve.
+lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward, int64_t chunk_tokens,
+                       Plan& p, bool query_device) {
+  if (N < 1 || H < 1 || V < 1 || !dtype_ok(dtype) || chunk_tokens < 0) return LCE_ERR_INVALID_ARGUMENT;
+  p.N = N; p.H = H; p.V = V;
+  p.esz = dtype == LCE_DTYPE_BF16 ? 2 : 4;
+  p.backward = backward;
+  if (H % (16 / p.esz) != 0) return LCE_ERR_UNSUPPORTED;
+  int64_t nc = chunk_tokens == 0 ? auto_chunk(N, H) : chunk_tokens;
+  if (nc >= N) nc = N;
+  else if (nc % 64 != 0) return LCE_ERR_INVALID_ARGUMENT;
+  p.nc = nc;
+  p.chunks = cdiv(N, nc);
+  p.Vp = round_up(V, 128);
+  p.ncp = round_up(nc, 64);
+  p.Np = round_up(N, 64);
+  p.slices = cdiv(V, kLseSlice);
+  // 32-bit limits: buffer ranges of one 256-row operand slice, and int tile/element indices.
+  const int64_t lim = (int64_t(1) << 31) - 1;
+  const int64_t maxpitch = std::max({H, p.Vp, p.ncp, p.Np});
+  if ((int64_t)kTile * maxpitch * p.esz > lim || N > lim / 2 || V > lim / 2 || H > lim / 2) return LCE_ERR_UNSUPPORTED;
+  if (cdiv(V, kTile) * cdiv(H, kTile) > lim / 16 || cdiv(p.Vp, 128) > 65535 || cdiv(p.ncp, 64) > 65535) return LCE_ERR_UNSUPPORTED;
+
+  if (backward) {
+    // dH tiles of one chunk: split the vocabulary (K) so that the grid fills the device.
+    const int64_t tiles = cdiv(nc, kTile) * cdiv(H, kTile);
+    const int cus = query_device ? num_cus() : 256;
+    const int64_t kbk = kRowBytes / p.esz;
+    const int64_t kblocks = cdiv(p.Vp, kbk);
+    double best = 1e30;
+    int best_s = 1;
+    for (int s = 1; s <= 8; ++s) {
+      if (s > kblocks) break;
+      const double waves = (double)cdiv(tiles * s, cus);
+      const double cost = waves / s + (s > 1 ? 0.03 * s : 0.0);
+      if (cost < best - 1e-9) { best = cost; best_s = s; }
+    }
+    p.dh_splits = best_s;
+    p.dh_kps = cdiv(kblocks, best_s) * kbk;
+  }
+
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (size_t)round_up((int64_t)bytes, kAlign);
+    return o;
+  };
+  p.o_nvalid = take(64);
+  p.o_tgt = take((size_t)N * 4);
+  p.o_lse = take((size_t)N * 4);
+  p.o_tl = take((size_t)N * 4);
+  p.o_pmax = take((size_t)p.slices * p.ncp * 4);
+  p.o_psum = take((size_t)p.slices * p.ncp * 4);
+  if (backward) {
+    p.o_e = take((size_t)p.ncp * p.Vp * p.esz);
+    p.o_zt = take((size_t)p.Vp * p.ncp * p.esz);
+    p.o_wt = take((size_t)H * p.Vp * p.esz);
+    p.o_xt = take((size_t)H * p.Np * p.esz);
+    if (p.chunks > 1) p.o_acc = take((size_t)V * H * 4);
+    if (p.dh_splits > 1) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
+  }
+  p.total = off;
+  return LCE_OK;
+}
+
+template <typename T, int EPI>
+hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
+  static std::atomic<uint64_t> configured[kMaxDevices / 64 + 1];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < kMaxDevices) {
+    const uint64_t bit = uint64_t(1) << (dev & 63);
+    if (!(configured[dev >> 6].load() & bit)) {
+      e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              kGemmSmem);
+      if (e != hipSuccess) return e;
+      configured[dev >> 6].fetch_or(bit);
+    }
+  }
+  g.tiles_m = (int)cdiv(g.M, kTile);
+  g.tiles_n = (int)cdiv(g.N, kTile);
+  const int blocks = g.tiles_m * g.tiles_n * g.splits;
+  if (blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_kernel<T, EPI>), dim3(blocks), dim3(kGemmThreads), kGemmSmem, s, g);
+  return hipGetLastError();
+}
+
+template <typename T>
+lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_t ignore_index, int reduction,
+                 float* loss, float* lse_user, T* dH, T* dW, char* ws, hipStream_t s) {
+  const int64_t N = p.N, H = p.H, V = p.V;
+  int* nvalid = (int*)(ws + p.o_nvalid);
+  float* tgt = (float*)(ws + p.o_tgt);
+  float* lse = lse_user ? lse_user : (float*)(ws + p.o_lse);
+  float* tl = (reduction == LCE_REDUCTION_NONE) ? loss : (float*)(ws + p.o_tl);
+  float* pmax = (float*)(ws + p.o_pmax);
+  float* psum = (float*)(ws + p.o_psum);
+  T* ez = p.backward ? (T*)(ws + p.o_e) : nullptr;
+  T* zt = p.backward ? (T*)(ws + p.o_zt) : nullptr;
+  T* wt = p.backward ? (T*)(ws + p.o_wt) : nullptr;
+  T* xt = p.backward ? (T*)(ws + p.o_xt) : nullptr;
+  float* acc = (p.backward && p.chunks > 1) ? (float*)(ws + p.o_acc) : nullptr;
+  float* dhp = (p.backward && p.dh_splits > 1) ? (float*)(ws + p.o_dhp) : nullptr;
+  const int mean = reduction == LCE_REDUCTION_MEAN;
+  const int64_t kChunk = 16 / p.esz;
+
+  {
+    KernelTimer t(T_OTHER, s);
+    hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(1024), 0, s, y, N, ignore_index, nvalid);
+    hipLaunchKernelGGL((target_logit_kernel<T>), dim3((unsigned)cdiv(N, 4)), dim3(256), 0, s, X, W, y, N, H, V,
+                       ignore_index, tgt);
+  }
+  if (p.backward) {
+    KernelTimer t(T_TRANSPOSE, s);
+    // W^T [H, Vp] and X^T [H, Np], zero-padded: the K-contiguous operands of the dH and dW GEMMs.
+    hipLaunchKernelGGL((transpose_kernel<T>), dim3((unsigned)cdiv(H, 64), (unsigned)cdiv(p.Vp, 64)), dim3(256), 0, s,
+                       W, H, V, H, wt, p.Vp, p.Vp);
+    hipLaunchKernelGGL((transpose_kernel<T>), dim3((unsigned)cdiv(H, 64), (unsigned)cdiv(p.Np, 64)), dim3(256), 0, s,
+                       X, H, N, H, xt, p.Np, p.Np);
+  }
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return LCE_ERR_HIP;
+
+  for (int64_t c = 0; c < p.chunks; ++c) {
+    const int64_t t0 = c * p.nc;
+    const int rows = (int)std::min(p.nc, N - t0);
+
+    // logits^T tile = W . X_c^T with the log-sum-exp epilogue.
+    GemmArgs g{};
+    g.A = W; g.lda = H; g.M = (int)V;
+    g.B = X + t0 * H; g.ldb = H; g.N = rows;
+    g.K = (int)H;
+    g.splits = 1; g.k_per_split = (int)round_up(H, kRowBytes / p.esz);
+    g.group_m = 4;
+    g.pmax = pmax; g.psum = psum; g.ldp = p.ncp;
+    hipError_t e;
+    {
+    KernelTimer t(T_LOGITS, s);
+    if (p.backward) {
+      g.out = ez; g.ldo = p.Vp;
+      e = launch_gemm<T, EPI_LSE_BWD>(g, s);
+    } else {
+      e = launch_gemm<T, EPI_LSE_FWD>(g, s);
+    }
+    }
+    if (e != hipSuccess) return LCE_ERR_HIP;
+
+    {
+    KernelTimer t(T_OTHER, s);
+    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)cdiv(rows, 32)), dim3(256), 0, s, pmax, psum, p.ncp,
+                       (int)p.slices, rows, y + t0, ignore_index, tgt + t0, lse + t0, tl + t0);
+    }
+    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+    if (!p.backward) continue;
+
+    // dlogits, in place (token-major) and transposed (vocabulary-major).
+    {
+    KernelTimer t(T_DLOGITS, s);
+    hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)(p.Vp / 128), (unsigned)(p.ncp / 64)), dim3(256), 0, s,
+                       ez, p.Vp, zt, p.ncp, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V);
+    }
+    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+
+    // dH rows of the chunk = dZ_c . W  (A = dZ_c [rows, Vp], B = W^T [H, Vp]).
+    GemmArgs gh{};
+    gh.A = ez; gh.lda = p.Vp; gh.M = rows;
+    gh.B = wt; gh.ldb = p.Vp; gh.N = (int)H;
+    gh.K = (int)round_up(V, kChunk);
+    gh.splits = p.dh_splits; gh.k_per_split = (int)p.dh_kps;
+    gh.group_m = 4;
+    if (p.dh_splits > 1) {
+      gh.out = dhp; gh.ldo = H; gh.mode = 1;
+    } else {
+      gh.out = dH + t0 * H; gh.ldo = H; gh.mode = 0;
+    }
+    {
+    KernelTimer t(T_DH, s);
+    if (launch_gemm<T, EPI_STORE>(gh, s) != hipSuccess) return LCE_ERR_HIP;
+    if (p.dh_splits > 1) {
+      const int64_t count = (int64_t)rows * H;
+      hipLaunchKernelGGL((split_reduce_kernel<T>), dim3((unsigned)cdiv(count / 4, 256)), dim3(256), 0, s, dhp,
+                         p.dh_splits, count, dH + t0 * H);
+      if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+    }
+    }
+
+    // dW += dZ_c^T . X_c  (A = dZ^T [V, ncp], B = X^T columns of the chunk [H, Np]).
+    GemmArgs gw{};
+    gw.A = zt; gw.lda = p.ncp; gw.M = (int)V;
+    gw.B = xt + t0; gw.ldb = p.Np; gw.N = (int)H;
+    gw.K = (int)round_up(rows, kChunk);
+    gw.splits = 1; gw.k_per_split = (int)round_up(gw.K, kRowBytes / p.esz);
+    gw.group_m = 4;
+    gw.out = dW; gw.ldo = H; gw.acc = acc; gw.ldacc = H;
+    gw.mode = p.chunks == 1 ? DW_ONLY : (c == 0 ? DW_FIRST : (c == p.chunks - 1 ? DW_LAST : DW_MID));
+    {
+    KernelTimer t(T_DW, s);
+    if (launch_gemm<T, EPI_DW>(gw, s) != hipSuccess) return LCE_ERR_HIP;
+    }
+  }
+
+  if (reduction != LCE_REDUCTION_NONE) {
+    KernelTimer t(T_OTHER, s);
+    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, s, tl, N, nvalid, mean, loss);
+  }
+  return hipGetLastError() == hipSuccess ? LCE_OK : LCE_ERR_HIP;
+}
+
+}  // namespace
+}  // namespace lce
+
+extern "C" {
+
+size_t lce_workspace_size(int64_t N, int64_t H, int64_t V, int dtype, int with_backward, int64_t chunk_tokens) {
+  lce::Plan p;
+  if (lce::make_plan(N, H, V, dtype, with_backward != 0, chunk_tokens, p, true) != LCE_OK) return 0;
+  return p.total;
+}
+
+int64_t lce_auto_chunk_tokens(int64_t N, int64_t H, int64_t V, int dtype) {
+  lce::Plan p;
+  if (lce::make_plan(N, H, V, dtype, true, 0, p, false) != LCE_OK) return 0;
+  return p.nc;
+}
+
+lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* labels, int64_t N, int64_t H,
+                         int64_t V, int dtype, int64_t ignore_index, int reduction, float* loss, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!hidden || !weight || !labels || !loss) return LCE_ERR_INVALID_ARGUMENT;
+  if (reduction != LCE_REDUCTION_NONE && reduction != LCE_REDUCTION_MEAN && reduction != LCE_REDUCTION_SUM)
+    return LCE_ERR_INVALID_ARGUMENT;
+  lce::Plan p;
+  lce_status_t st = lce::make_plan(N, H, V, dtype, false, 0, p, true);
+  if (st != LCE_OK) return st;
+  if (!workspace || workspace_bytes < p.total) return LCE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LCE_DTYPE_BF16)
+    return lce::run<lce::bf16>(p, (const lce::bf16*)hidden, (const lce::bf16*)weight, labels, ignore_index,
+                               reduction, loss, lse, nullptr, nullptr, (char*)workspace, s);
+  return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss, lse,
+                         nullptr, nullptr, (char*)workspace, s);
+}
+
+lce_status_t lce_forward_backward(const void* hidden, const void* weight, const int64_t* labels, int64_t N,
+                                  int64_t H, int64_t V, int dtype, int64_t ignore_index, int reduction, float* loss,
+                                  void* grad_hidden, void* grad_weight, int64_t chunk_tokens, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  if (!hidden || !weight || !labels || !loss || !grad_hidden || !grad_weight) return LCE_ERR_INVALID_ARGUMENT;
+  if (reduction != LCE_REDUCTION_MEAN && reduction != LCE_REDUCTION_SUM) return LCE_ERR_INVALID_ARGUMENT;
+  lce::Plan p;
+  lce_status_t st = lce::make_plan(N, H, V, dtype, true, chunk_tokens, p, true);
+  if (st != LCE_OK) return st;
+  if (!workspace || workspace_bytes < p.total) return LCE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LCE_DTYPE_BF16)
+    return lce::run<lce::bf16>(p, (const lce::bf16*)hidden, (const lce::bf16*)weight, labels, ignore_index,
+                               reduction, loss, nullptr, (lce::bf16*)grad_hidden, (lce::bf16*)grad_weight,
+                               (char*)workspace, s);
+  return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss,
+                         nullptr, (float*)grad_hidden, (float*)grad_weight, (char*)workspace, s);
+}
+
+lce_status_t lce_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(lce::g_timing_mu);
+  for (auto& t : lce::g_timed) {
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  lce::g_timed.clear();
+  lce::g_timing_on = enable != 0;
+  return LCE_OK;
+}
+
+lce_status_t lce_timing_read(double* ms, int64_t* launches, int n_kinds) {
+  if (!ms || !launches || n_kinds < 1) return LCE_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lk(lce::g_timing_mu);
+  for (int k = 0; k < n_kinds; ++k) { ms[k] = 0.0; launches[k] = 0; }
+  lce_status_t st = LCE_OK;
+  for (auto& t : lce::g_timed) {
+    float e = 0.f;
+    if (hipEventSynchronize(t.stop) != hipSuccess || hipEventElapsedTime(&e, t.start, t.stop) != hipSuccess) {
+      st = LCE_ERR_HIP;
+    } else if (t.kind < n_kinds) {
+      ms[t.kind] += e;
+      launches[t.kind] += 1;
+    }
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  lce::g_timed.clear();
+  return st;
+}
+
+const char* lce_status_string(int status) {
+  switch (status) {
+    case LCE_OK: return "LCE_OK";
+    case LCE_ERR_INVALID_ARGUMENT: return "LCE_ERR_INVALID_ARGUMENT";
+    case LCE_ERR_UNSUPPORTED: return "LCE_ERR_UNSUPPORTED";
+    case LCE_ERR_WORKSPACE_TOO_SMALL: return "LCE_ERR_WORKSPACE_TOO_SMALL";
+    case LCE_ERR_HIP: return "LCE_ERR_HIP";
+    default: return "LCE_ERR_UNKNOWN";
+  }
+}
+
+}  // extern "C"

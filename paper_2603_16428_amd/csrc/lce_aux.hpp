@@ -1,0 +1,224 @@
+// Bandwidth-bound kernels around the three contractions of the fused linear + cross-entropy step.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lce_gemm.hpp"
+
+namespace lce {
+
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+__device__ __forceinline__ float to_f32(float v) { return v; }
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+
+// n_valid = number of labels different from ignore_index, over all N tokens (the mean's divisor
+// is global, never per chunk). One block of 1024 threads; fixed-order tree, so deterministic.
+__global__ __launch_bounds__(1024) void count_valid_kernel(const int64_t* __restrict__ y, int64_t N,
+                                                           int64_t ignore_index, int* __restrict__ n_valid) {
+  __shared__ int part[1024];
+  int c = 0;
+  for (int64_t i = threadIdx.x; i < N; i += 1024) c += (y[i] != ignore_index);
+  part[threadIdx.x] = c;
+  __syncthreads();
+  for (int s = 512; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *n_valid = part[0];
+}
+
+// Target logit z_{i, y_i} = x_i . w_{y_i} in fp32, one wave per token. Ignored tokens get 0;
+// a label outside [0, V) gets NaN (so that the token's loss is NaN) and reads nothing.
+template <typename T>
+__global__ __launch_bounds__(256) void target_logit_kernel(const T* __restrict__ X, const T* __restrict__ W,
+                                                           const int64_t* __restrict__ y, int64_t N, int64_t H,
+                                                           int64_t V, int64_t ignore_index, float* __restrict__ tgt) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  const int64_t lab = y[i];
+  if (lab == ignore_index) {
+    if (lane == 0) tgt[i] = 0.f;
+    return;
+  }
+  if (lab < 0 || lab >= V) {
+    if (lane == 0) tgt[i] = __builtin_nanf("");
+    return;
+  }
+  constexpr int kVec = 16 / sizeof(T);
+  const T* xr = X + i * H;
+  const T* wr = W + lab * H;
+  float s = 0.f;
+  for (int64_t h = (int64_t)lane * kVec; h < H; h += 64 * kVec) {
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) s = fmaf(to_f32(xr[h + e]), to_f32(wr[h + e]), s);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) tgt[i] = s;
+}
+
+// Row combine. For each token of the chunk: M = max_t m_t, lse = M + log sum_t s_t exp(m_t - M),
+// and the token loss lse - z_target (0 for ignored tokens). 32 tokens x 8 slice-groups per block;
+// each thread merges its slices in increasing order, then the 8 groups merge in a fixed order.
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ pmax, const float* __restrict__ psum,
+                                                      int64_t ldp, int slices, int rows,
+                                                      const int64_t* __restrict__ y, int64_t ignore_index,
+                                                      const float* __restrict__ tgt,
+                                                      float* __restrict__ lse_out,     // [rows] (chunk-offset)
+                                                      float* __restrict__ loss_out) {  // [rows] (chunk-offset)
+  __shared__ float sm[8][32], ss[8][32];
+  const int t = threadIdx.x & 31, gidx = threadIdx.x >> 5;
+  const int i = blockIdx.x * 32 + t;
+  float m = -INFINITY, s = 0.f;
+  if (i < rows) {
+    for (int k = gidx; k < slices; k += 8) {
+      const float mk = pmax[(size_t)k * ldp + i], sk = psum[(size_t)k * ldp + i];
+      const float mn = fmaxf(m, mk);
+      s = s * __expf(m - mn) + sk * __expf(mk - mn);
+      m = mn;
+    }
+  }
+  sm[gidx][t] = m;
+  ss[gidx][t] = s;
+  __syncthreads();
+  if (gidx == 0 && i < rows) {
+    float M = sm[0][t];
+    for (int k = 1; k < 8; ++k) M = fmaxf(M, sm[k][t]);
+    float S = 0.f;
+    for (int k = 0; k < 8; ++k) S += ss[k][t] * __expf(sm[k][t] - M);
+    const float lse = M + __logf(S);
+    lse_out[i] = lse;
+    loss_out[i] = (y[i] == ignore_index) ? 0.f : lse - tgt[i];
+  }
+}
+
+// dlogits. For token i of the chunk and vocabulary id v (slice t = v / 128):
+//   dZ[i][v] = g_i exp(m_t,i - lse_i) e[i][v] - g_i [v == y_i],   g_i = valid_i / n_valid (mean) or valid_i.
+// e (token-major, pitch ldz) is overwritten with dZ; dZ^T (vocabulary-major, pitch ldt) is written
+// through an LDS transpose. Entries outside the valid tokens / vocabulary but inside the pitches
+// are written as zeros (the contractions read them as padding). Tile: 64 tokens x 128 ids.
+template <typename T>
+__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t ldz, T* __restrict__ zt,
+                                                      int64_t ldt, const float* __restrict__ pmax,
+                                                      int64_t ldp, const float* __restrict__ lse,
+                                                      const int64_t* __restrict__ y, int64_t ignore_index,
+                                                      const int* __restrict__ n_valid, int mean, int rows,
+                                                      int V) {
+  constexpr int kVec = 16 / sizeof(T);          // elements per 16-byte access
+  constexpr int kTpr = 128 / kVec;              // threads per 128-id row
+  constexpr int kRowsPerPass = 256 / kTpr;
+  __shared__ T tile[64][128 + 8 / sizeof(T) * 2];
+  const int v0 = blockIdx.x * 128, i0 = blockIdx.y * 64;
+  const int slice = blockIdx.x;
+  const int nv = *n_valid;
+  const float gscale = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
+  const int tc = threadIdx.x % kTpr, tr = threadIdx.x / kTpr;
+  for (int r = tr; r < 64; r += kRowsPerPass) {
+    const int i = i0 + r;
+    const int v = v0 + tc * kVec;
+    T outv[kVec];
+    bool valid_tok = i < rows;
+    int64_t lab = valid_tok ? y[i] : ignore_index;
+    const bool valid = valid_tok && lab != ignore_index;
+    if (valid) {
+      const float g = gscale;
+      const float c = g * __expf(pmax[(size_t)slice * ldp + i] - lse[i]);
+      T ev[kVec];
+      *(uint4*)ev = *(const uint4*)(ez + (size_t)i * ldz + v);
+#pragma unroll
+      for (int e = 0; e < kVec; ++e) {
+        float d = (v + e < V) ? c * to_f32(ev[e]) : 0.f;
+        if (v + e == lab) d -= g;
+        outv[e] = from_f32<T>(d);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < kVec; ++e) outv[e] = from_f32<T>(0.f);
+    }
+    // Rows beyond the chunk are written as zeros too: they are padding of dZ^T's columns.
+    *(uint4*)(ez + (size_t)i * ldz + v) = *(const uint4*)outv;
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) tile[r][tc * kVec + e] = outv[e];
+  }
+  __syncthreads();
+  // Transposed write: row v of dZ^T gets 64 tokens = 64 * sizeof(T) bytes.
+  constexpr int kTprT = 64 / kVec;              // threads per dZ^T row segment
+  constexpr int kRowsPerPassT = 256 / kTprT;
+  const int tcT = threadIdx.x % kTprT, trT = threadIdx.x / kTprT;
+  for (int r = trT; r < 128; r += kRowsPerPassT) {
+    T outv[kVec];
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) outv[e] = tile[tcT * kVec + e][r];
+    *(uint4*)(zt + (size_t)(v0 + r) * ldt + i0 + tcT * kVec) = *(const uint4*)outv;
+  }
+}
+
+// out[c][r] = in[r][c] for r < R, c < C; columns r in [R, Rp) of out are zero-filled.
+// in: [R, ldi], out: [C, ldo] with ldo >= Rp. Tile 64 x 64 through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int64_t ldi, int64_t R, int64_t C,
+                                                        T* __restrict__ out, int64_t ldo, int64_t Rp) {
+  __shared__ T tile[64][64 + 1];
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int k = ty; k < 64; k += 4) {
+    const int64_t r = r0 + k, c = c0 + tx;
+    tile[k][tx] = (r < R && c < C) ? in[r * ldi + c] : from_f32<T>(0.f);
+  }
+  __syncthreads();
+  for (int k = ty; k < 64; k += 4) {
+    const int64_t c = c0 + k, r = r0 + tx;
+    if (c < C && r < Rp) out[c * ldo + r] = tile[tx][k];
+  }
+}
+
+// out[i][h] = sum_s part[s][i][h] (fixed order), converted to the output type.
+template <typename T>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int splits,
+                                                           int64_t count, T* __restrict__ out) {
+  const int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (idx >= count) return;
+  float4 s = *(const float4*)(part + idx);
+  for (int k = 1; k < splits; ++k) {
+    const float4 v = *(const float4*)(part + (size_t)k * count + idx);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  out[idx] = from_f32<T>(s.x);
+  out[idx + 1] = from_f32<T>(s.y);
+  out[idx + 2] = from_f32<T>(s.z);
+  out[idx + 3] = from_f32<T>(s.w);
+}
+
+// Final reduction of the token losses: sum in fp64 with a fixed-order tree, divided by n_valid for
+// the mean (0 when no token is valid).
+__global__ __launch_bounds__(1024) void loss_reduce_kernel(const float* __restrict__ tl, int64_t N,
+                                                           const int* __restrict__ n_valid, int mean,
+                                                           float* __restrict__ loss) {
+  __shared__ double part[1024];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < N; i += 1024) s += (double)tl[i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int k = 512; k > 0; k >>= 1) {
+    if ((int)threadIdx.x < k) part[threadIdx.x] += part[threadIdx.x + k];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    double r = part[0];
+    if (mean) {
+      const int nv = *n_valid;
+      r = nv > 0 ? r / (double)nv : 0.0;
+    }
+    *loss = (float)r;
+  }
+}
+
+__global__ void zero_kernel(float* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+}  // namespace lce

@@ -1,0 +1,189 @@
+"""Python binding of the C ABI in include/lce.h (argument marshalling only).
+
+Every step of the fused linear + cross-entropy computation runs in the HIP
+kernels of liblce.so; this module allocates the outputs and the workspace with
+torch (device memory and streams are all torch is used for) and passes raw
+pointers. There is no fallback: if the library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblce.so")
+
+LCE_OK = 0
+STATUS = {0: "LCE_OK", 1: "LCE_ERR_INVALID_ARGUMENT", 2: "LCE_ERR_UNSUPPORTED",
+          3: "LCE_ERR_WORKSPACE_TOO_SMALL", 4: "LCE_ERR_HIP"}
+DTYPES = {torch.float32: 0, torch.bfloat16: 1}
+REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
+EXPORTED = ("lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
+            "lce_timing_enable", "lce_timing_read", "lce_status_string")
+TIMING_KINDS = ("logits_lse_gemm", "dh_gemm", "dw_gemm", "dlogits", "transpose", "other")
+
+_lib = None
+
+
+class LCEError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load liblce.so and declare its signatures. Raises OSError if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise OSError(f"{path} is not built; run `python -m paper_2603_16428_amd.build`")
+    lib = ctypes.CDLL(path)
+    i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+    lib.lce_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, ctypes.c_int, i64]
+    lib.lce_workspace_size.restype = sz
+    lib.lce_auto_chunk_tokens.argtypes = [i64, i64, i64, ctypes.c_int]
+    lib.lce_auto_chunk_tokens.restype = i64
+    lib.lce_forward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp, sz, vp]
+    lib.lce_forward.restype = ctypes.c_int
+    lib.lce_forward_backward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp,
+                                         i64, vp, sz, vp]
+    lib.lce_forward_backward.restype = ctypes.c_int
+    lib.lce_timing_enable.argtypes = [ctypes.c_int]
+    lib.lce_timing_enable.restype = ctypes.c_int
+    lib.lce_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
+    lib.lce_timing_read.restype = ctypes.c_int
+    lib.lce_status_string.argtypes = [ctypes.c_int]
+    lib.lce_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def timing_enable(enable: bool = True) -> None:
+    """Start (and reset) or stop per-kernel event timing inside the library."""
+    st = load_library().lce_timing_enable(int(enable))
+    if st != LCE_OK:
+        raise LCEError(st, "lce_timing_enable")
+
+
+def timing_read() -> dict:
+    """{kind: (total_ms, launches)} since the last timing_enable(True); waits for the events."""
+    n = len(TIMING_KINDS)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    st = load_library().lce_timing_read(ms, cnt, n)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_timing_read")
+    return {k: (ms[i], int(cnt[i])) for i, k in enumerate(TIMING_KINDS)}
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check_inputs(hidden, weight, labels):
+    if not (hidden.is_cuda and weight.is_cuda and labels.is_cuda):
+        raise ValueError("hidden, weight and labels must be device tensors")
+    if hidden.dim() != 2 or weight.dim() != 2 or labels.dim() != 1:
+        raise ValueError("expected hidden [N,H], weight [V,H], labels [N]")
+    if hidden.dtype != weight.dtype or hidden.dtype not in DTYPES:
+        raise ValueError("hidden and weight must both be bfloat16 or both float32")
+    if labels.dtype != torch.int64:
+        raise ValueError("labels must be int64")
+    N, H = hidden.shape
+    V, H2 = weight.shape
+    if H2 != H or labels.shape[0] != N:
+        raise ValueError("shape mismatch")
+    if not (hidden.is_contiguous() and weight.is_contiguous() and labels.is_contiguous()):
+        raise ValueError("inputs must be contiguous")
+    return N, H, V
+
+
+def workspace_size(N: int, H: int, V: int, dtype=torch.bfloat16, with_backward: bool = True,
+                   chunk_tokens: int = 0) -> int:
+    return int(load_library().lce_workspace_size(N, H, V, DTYPES[dtype], int(with_backward), chunk_tokens))
+
+
+def auto_chunk_tokens(N: int, H: int, V: int, dtype=torch.bfloat16) -> int:
+    return int(load_library().lce_auto_chunk_tokens(N, H, V, DTYPES[dtype]))
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def forward(hidden, weight, labels, ignore_index: int = -100, reduction: str = "mean",
+            return_lse: bool = False, workspace: torch.Tensor | None = None):
+    """Loss (scalar for mean/sum, [N] for none) and optionally each token's log-sum-exp."""
+    lib = load_library()
+    N, H, V = _check_inputs(hidden, weight, labels)
+    dt = DTYPES[hidden.dtype]
+    red = REDUCTIONS[reduction]
+    need = lib.lce_workspace_size(N, H, V, dt, 0, 0)
+    if need == 0:
+        raise LCEError(2, "lce_workspace_size")
+    ws = workspace if workspace is not None else _workspace(need, hidden.device)
+    loss = torch.empty(N if red == 0 else 1, dtype=torch.float32, device=hidden.device)
+    lse = torch.empty(N, dtype=torch.float32, device=hidden.device) if return_lse else None
+    stream = ctypes.c_void_p(torch.cuda.current_stream(hidden.device).cuda_stream)
+    st = lib.lce_forward(_ptr(hidden), _ptr(weight), _ptr(labels), N, H, V, dt, ignore_index, red,
+                         _ptr(loss), _ptr(lse), _ptr(ws), ws.numel(), stream)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_forward")
+    loss = loss if red == 0 else loss[0]
+    return (loss, lse) if return_lse else loss
+
+
+def forward_backward(hidden, weight, labels, ignore_index: int = -100, reduction: str = "mean",
+                     chunk_tokens: int = 0, workspace: torch.Tensor | None = None,
+                     out: tuple | None = None):
+    """(loss, grad_hidden, grad_weight) of the mean or sum loss, upstream gradient 1."""
+    lib = load_library()
+    N, H, V = _check_inputs(hidden, weight, labels)
+    dt = DTYPES[hidden.dtype]
+    red = REDUCTIONS[reduction]
+    need = lib.lce_workspace_size(N, H, V, dt, 1, chunk_tokens)
+    if need == 0:
+        raise LCEError(2, "lce_workspace_size")
+    ws = workspace if workspace is not None else _workspace(need, hidden.device)
+    if out is None:
+        loss = torch.empty(1, dtype=torch.float32, device=hidden.device)
+        dH = torch.empty_like(hidden)
+        dW = torch.empty_like(weight)
+    else:
+        loss, dH, dW = out
+    stream = ctypes.c_void_p(torch.cuda.current_stream(hidden.device).cuda_stream)
+    st = lib.lce_forward_backward(_ptr(hidden), _ptr(weight), _ptr(labels), N, H, V, dt, ignore_index, red,
+                                  _ptr(loss), _ptr(dH), _ptr(dW), chunk_tokens, _ptr(ws), ws.numel(), stream)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_forward_backward")
+    return loss[0], dH, dW
+
+
+class LinearCrossEntropy(torch.autograd.Function):
+    """loss = cross_entropy(hidden @ weight.T, labels) without the logits tensor.
+
+    The forward pass computes the gradients too (they come out of the same chunked pass) and the
+    backward pass only scales them by the upstream gradient.
+    """
+
+    @staticmethod
+    def forward(ctx, hidden, weight, labels, ignore_index=-100, reduction="mean"):
+        if hidden.requires_grad or weight.requires_grad:
+            loss, dH, dW = forward_backward(hidden, weight, labels, ignore_index, reduction)
+            ctx.save_for_backward(dH, dW)
+        else:
+            loss = forward(hidden, weight, labels, ignore_index, reduction)
+        return loss
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        dH, dW = ctx.saved_tensors
+        g = grad_out.to(torch.float32)
+        return (dH * g).to(dH.dtype), (dW * g).to(dW.dtype), None, None, None
+
+
+def linear_cross_entropy(hidden, weight, labels, ignore_index: int = -100, reduction: str = "mean"):
+    return LinearCrossEntropy.apply(hidden, weight, labels, ignore_index, reduction)

@@ -1,0 +1,107 @@
+"""The C ABI on the CPU: the library loads, exports every function include/lce.h declares, and
+rejects invalid arguments before it touches the GPU. No case here passes validation, so nothing
+is ever launched (the pointers below are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lce.h")
+
+OK, INVALID, UNSUPPORTED, WS_SMALL, HIP = 0, 1, 2, 3, 4
+BF16, FP32 = 1, 0
+NONE, MEAN, SUM = 0, 1, 2
+FAKE = ctypes.c_void_p(0x1000)  # non-null, never dereferenced: every call below fails validation
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2603_16428_amd import lce
+    return lce.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lce_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert names == sorted(["lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward",
+                            "lce_forward_backward", "lce_timing_enable", "lce_timing_read",
+                            "lce_status_string"])
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_names_match_header():
+    from paper_2603_16428_amd import lce
+    assert sorted(lce.EXPORTED) == _declared_functions()
+
+
+def test_status_strings(lib):
+    for code, name in [(0, b"LCE_OK"), (1, b"LCE_ERR_INVALID_ARGUMENT"), (2, b"LCE_ERR_UNSUPPORTED"),
+                       (3, b"LCE_ERR_WORKSPACE_TOO_SMALL"), (4, b"LCE_ERR_HIP"), (99, b"LCE_ERR_UNKNOWN")]:
+        assert lib.lce_status_string(code) == name
+
+
+def test_workspace_size(lib):
+    ws = lib.lce_workspace_size
+    assert ws(0, 8, 8, BF16, 1, 0) == 0
+    assert ws(8, 0, 8, BF16, 1, 0) == 0
+    assert ws(8, 8, 0, BF16, 1, 0) == 0
+    assert ws(8, 8, 8, 7, 1, 0) == 0
+    assert ws(8, 12, 8, BF16, 1, 0) == 0          # H not a multiple of 8 for bf16
+    assert ws(8, 12, 8, FP32, 1, 0) > 0           # fine for fp32
+    assert ws(300, 64, 100, BF16, 1, 100) == 0    # chunk must be a multiple of 64 when < N
+    fwd = ws(8192, 4096, 128256, BF16, 0, 0)
+    bwd = ws(8192, 4096, 128256, BF16, 1, 0)
+    assert 0 < fwd < bwd
+    # The workspace is O(n_c*V + V*H + N*H): at a fixed chunk size, doubling N adds only N*H-sized
+    # buffers, never another N*V of logits.
+    a = ws(8192, 4096, 128256, BF16, 1, 4096)
+    b = ws(16384, 4096, 128256, BF16, 1, 4096)
+    assert 0 < b - a <= 8192 * 4096 * 2 + 8192 * 64
+    assert lib.lce_auto_chunk_tokens(8192, 4096, 128256, BF16) == 4096
+    assert lib.lce_auto_chunk_tokens(16384, 3584, 152064, BF16) == 3584
+    assert lib.lce_auto_chunk_tokens(4096, 12288, 32768, BF16) == 2048
+    assert lib.lce_auto_chunk_tokens(37, 72, 1000, BF16) == 37  # one chunk
+
+
+def _fwd(lib, **kw):
+    a = dict(hidden=FAKE, weight=FAKE, labels=FAKE, N=16, H=64, V=100, dtype=BF16, ignore=-100,
+             red=MEAN, loss=FAKE, lse=None, ws=FAKE, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return lib.lce_forward(a["hidden"], a["weight"], a["labels"], a["N"], a["H"], a["V"], a["dtype"],
+                           a["ignore"], a["red"], a["loss"], a["lse"], a["ws"], a["wsb"], a["stream"])
+
+
+def _fb(lib, **kw):
+    a = dict(hidden=FAKE, weight=FAKE, labels=FAKE, N=16, H=64, V=100, dtype=BF16, ignore=-100,
+             red=MEAN, loss=FAKE, dh=FAKE, dw=FAKE, chunk=0, ws=FAKE, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return lib.lce_forward_backward(a["hidden"], a["weight"], a["labels"], a["N"], a["H"], a["V"],
+                                    a["dtype"], a["ignore"], a["red"], a["loss"], a["dh"], a["dw"],
+                                    a["chunk"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(hidden=None), INVALID), (dict(weight=None), INVALID), (dict(labels=None), INVALID),
+    (dict(loss=None), INVALID), (dict(N=0), INVALID), (dict(H=-1), INVALID), (dict(V=0), INVALID),
+    (dict(dtype=5), INVALID), (dict(red=3), INVALID), (dict(H=60), UNSUPPORTED),
+    (dict(ws=None), WS_SMALL), (dict(wsb=16), WS_SMALL),
+])
+def test_forward_validation(lib, kw, status):
+    assert _fwd(lib, **kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dh=None), INVALID), (dict(dw=None), INVALID), (dict(red=NONE), INVALID),
+    (dict(red=7), INVALID), (dict(chunk=-1), INVALID), (dict(N=300, chunk=100), INVALID),
+    (dict(H=20), UNSUPPORTED), (dict(wsb=0), WS_SMALL), (dict(ws=None), WS_SMALL),
+])
+def test_forward_backward_validation(lib, kw, status):
+    assert _fb(lib, **kw) == status
