@@ -2,12 +2,12 @@
 //
 // Per call (Section 3.3, "Optimized Triton Kernels": projection fused with the loss, gradients in
 // token chunks, the N x V logits never held):
-//   count valid labels (global mean divisor) -> target logits -> [backward: W^T, X^T]
+//   count valid labels (global mean divisor) -> target logits
 //   for each chunk of n_c tokens:
 //     logits^T tile GEMM with the log-sum-exp epilogue  (stores e = exp(z - m_slice) for backward)
 //     row combine -> lse, token losses
-//     [backward] dlogits (in place, plus its transpose) -> dH rows GEMM -> dW GEMM (fp32 accumulate
-//                across chunks in a fixed order; the last chunk writes the output dtype)
+//     [backward] dlogits in place -> dH rows GEMM (reads W as it is) -> dW GEMM (reads dZ and X
+//                as they are; the first chunk writes dW, later chunks add to it)
 //   loss reduction (fp64, fixed order)
 #include <hip/hip_runtime.h>
 
@@ -31,7 +31,7 @@ constexpr int kMaxDevices = 64;
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 // ---- optional per-kernel timing (events on the launch stream) ----
-enum TimingKind { T_LOGITS = 0, T_DH = 1, T_DW = 2, T_DLOGITS = 3, T_TRANSPOSE = 4, T_OTHER = 5, T_KINDS = 6 };
+enum TimingKind { T_LOGITS = 0, T_DH = 1, T_DW = 2, T_DLOGITS = 3, T_OTHER = 5, T_KINDS = 6 };
 struct TimedLaunch {
   int kind;
   hipEvent_t start, stop;
@@ -74,13 +74,12 @@ struct Plan {
   int esz = 0;
   bool backward = false;
   int64_t nc = 0, chunks = 0;     // tokens per chunk, number of chunks
-  int64_t Vp = 0, ncp = 0, Np = 0;
+  int64_t Vp = 0, ncp = 0;
   int64_t slices = 0;
   int dh_splits = 1;
   int64_t dh_kps = 0;             // K (vocabulary) per dH split, multiple of the K-tile
   // workspace offsets (bytes)
-  size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_zt = 0,
-         o_wt = 0, o_xt = 0, o_acc = 0, o_dhp = 0;
+  size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_dhp = 0;
   size_t total = 0;
 };
 
@@ -123,19 +122,18 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.chunks = cdiv(N, nc);
   p.Vp = round_up(V, 128);
   p.ncp = round_up(nc, 64);
-  p.Np = round_up(N, 64);
   p.slices = cdiv(V, kLseSlice);
   // 32-bit limits: buffer ranges of one 256-row operand slice, and int tile/element indices.
   const int64_t lim = (int64_t(1) << 31) - 1;
-  const int64_t maxpitch = std::max({H, p.Vp, p.ncp, p.Np});
+  const int64_t maxpitch = std::max({H, p.Vp});
   if ((int64_t)kTile * maxpitch * p.esz > lim || N > lim / 2 || V > lim / 2 || H > lim / 2) return LCE_ERR_UNSUPPORTED;
-  if (cdiv(V, kTile) * cdiv(H, kTile) > lim / 16 || cdiv(p.Vp, 128) > 65535 || cdiv(p.ncp, 64) > 65535) return LCE_ERR_UNSUPPORTED;
+  if (cdiv(V, kTile) * cdiv(H, kTile) > lim / 16 || cdiv(p.ncp * p.Vp, 2048) > lim) return LCE_ERR_UNSUPPORTED;
 
   if (backward) {
     // dH tiles of one chunk: split the vocabulary (K) so that the grid fills the device.
     const int64_t tiles = cdiv(nc, kTile) * cdiv(H, kTile);
     const int cus = query_device ? num_cus() : 256;
-    const int64_t kbk = kRowBytes / p.esz;
+    const int64_t kbk = kTileBytes / p.esz;
     const int64_t kblocks = cdiv(p.Vp, kbk);
     double best = 1e30;
     int best_s = 1;
@@ -163,17 +161,13 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.o_psum = take((size_t)p.slices * p.ncp * 4);
   if (backward) {
     p.o_e = take((size_t)p.ncp * p.Vp * p.esz);
-    p.o_zt = take((size_t)p.Vp * p.ncp * p.esz);
-    p.o_wt = take((size_t)H * p.Vp * p.esz);
-    p.o_xt = take((size_t)H * p.Np * p.esz);
-    if (p.chunks > 1) p.o_acc = take((size_t)V * H * 4);
     if (p.dh_splits > 1) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
   }
   p.total = off;
   return LCE_OK;
 }
 
-template <typename T, int EPI>
+template <typename T, int EPI, bool A_MN, bool B_MN>
 hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   static std::atomic<uint64_t> configured[kMaxDevices / 64 + 1];
   int dev = 0;
@@ -182,7 +176,7 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   if (dev < kMaxDevices) {
     const uint64_t bit = uint64_t(1) << (dev & 63);
     if (!(configured[dev >> 6].load() & bit)) {
-      e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI, A_MN, B_MN>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               kGemmSmem);
       if (e != hipSuccess) return e;
       configured[dev >> 6].fetch_or(bit);
@@ -192,7 +186,7 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   g.tiles_n = (int)cdiv(g.N, kTile);
   const int blocks = g.tiles_m * g.tiles_n * g.splits;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<T, EPI>), dim3(blocks), dim3(kGemmThreads), kGemmSmem, s, g);
+  hipLaunchKernelGGL((gemm_kernel<T, EPI, A_MN, B_MN>), dim3(blocks), dim3(kGemmThreads), kGemmSmem, s, g);
   return hipGetLastError();
 }
 
@@ -207,27 +201,14 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
   float* pmax = (float*)(ws + p.o_pmax);
   float* psum = (float*)(ws + p.o_psum);
   T* ez = p.backward ? (T*)(ws + p.o_e) : nullptr;
-  T* zt = p.backward ? (T*)(ws + p.o_zt) : nullptr;
-  T* wt = p.backward ? (T*)(ws + p.o_wt) : nullptr;
-  T* xt = p.backward ? (T*)(ws + p.o_xt) : nullptr;
-  float* acc = (p.backward && p.chunks > 1) ? (float*)(ws + p.o_acc) : nullptr;
   float* dhp = (p.backward && p.dh_splits > 1) ? (float*)(ws + p.o_dhp) : nullptr;
   const int mean = reduction == LCE_REDUCTION_MEAN;
-  const int64_t kChunk = 16 / p.esz;
 
   {
     KernelTimer t(T_OTHER, s);
     hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(1024), 0, s, y, N, ignore_index, nvalid);
     hipLaunchKernelGGL((target_logit_kernel<T>), dim3((unsigned)cdiv(N, 4)), dim3(256), 0, s, X, W, y, N, H, V,
                        ignore_index, tgt);
-  }
-  if (p.backward) {
-    KernelTimer t(T_TRANSPOSE, s);
-    // W^T [H, Vp] and X^T [H, Np], zero-padded: the K-contiguous operands of the dH and dW GEMMs.
-    hipLaunchKernelGGL((transpose_kernel<T>), dim3((unsigned)cdiv(H, 64), (unsigned)cdiv(p.Vp, 64)), dim3(256), 0, s,
-                       W, H, V, H, wt, p.Vp, p.Vp);
-    hipLaunchKernelGGL((transpose_kernel<T>), dim3((unsigned)cdiv(H, 64), (unsigned)cdiv(p.Np, 64)), dim3(256), 0, s,
-                       X, H, N, H, xt, p.Np, p.Np);
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return LCE_ERR_HIP;
 
@@ -240,7 +221,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     g.A = W; g.lda = H; g.M = (int)V;
     g.B = X + t0 * H; g.ldb = H; g.N = rows;
     g.K = (int)H;
-    g.splits = 1; g.k_per_split = (int)round_up(H, kRowBytes / p.esz);
+    g.splits = 1; g.k_per_split = (int)round_up(H, kTileBytes / p.esz);
     g.group_m = 4;
     g.pmax = pmax; g.psum = psum; g.ldp = p.ncp;
     hipError_t e;
@@ -248,9 +229,9 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     KernelTimer t(T_LOGITS, s);
     if (p.backward) {
       g.out = ez; g.ldo = p.Vp;
-      e = launch_gemm<T, EPI_LSE_BWD>(g, s);
+      e = launch_gemm<T, EPI_LSE_BWD, false, false>(g, s);
     } else {
-      e = launch_gemm<T, EPI_LSE_FWD>(g, s);
+      e = launch_gemm<T, EPI_LSE_FWD, false, false>(g, s);
     }
     }
     if (e != hipSuccess) return LCE_ERR_HIP;
@@ -263,19 +244,19 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
     if (!p.backward) continue;
 
-    // dlogits, in place (token-major) and transposed (vocabulary-major).
+    // dlogits, in place.
     {
     KernelTimer t(T_DLOGITS, s);
     hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)(p.Vp / 128), (unsigned)(p.ncp / 64)), dim3(256), 0, s,
-                       ez, p.Vp, zt, p.ncp, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V);
-    }
+                       ez, p.Vp, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V);
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+    }
 
-    // dH rows of the chunk = dZ_c . W  (A = dZ_c [rows, Vp], B = W^T [H, Vp]).
+    // dH rows of the chunk = dZ_c . W  (A = dZ_c [rows, Vp] K-contig, B = W [V, H] MN-contig).
     GemmArgs gh{};
     gh.A = ez; gh.lda = p.Vp; gh.M = rows;
-    gh.B = wt; gh.ldb = p.Vp; gh.N = (int)H;
-    gh.K = (int)round_up(V, kChunk);
+    gh.B = W; gh.ldb = H; gh.N = (int)H;
+    gh.K = (int)V;
     gh.splits = p.dh_splits; gh.k_per_split = (int)p.dh_kps;
     gh.group_m = 4;
     if (p.dh_splits > 1) {
@@ -285,7 +266,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     }
     {
     KernelTimer t(T_DH, s);
-    if (launch_gemm<T, EPI_STORE>(gh, s) != hipSuccess) return LCE_ERR_HIP;
+    if (launch_gemm<T, EPI_STORE, false, true>(gh, s) != hipSuccess) return LCE_ERR_HIP;
     if (p.dh_splits > 1) {
       const int64_t count = (int64_t)rows * H;
       hipLaunchKernelGGL((split_reduce_kernel<T>), dim3((unsigned)cdiv(count / 4, 256)), dim3(256), 0, s, dhp,
@@ -294,18 +275,18 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     }
     }
 
-    // dW += dZ_c^T . X_c  (A = dZ^T [V, ncp], B = X^T columns of the chunk [H, Np]).
+    // dW (+)= dZ_c^T . X_c  (A = dZ_c MN-contig over the vocabulary, B = X_c MN-contig over H).
     GemmArgs gw{};
-    gw.A = zt; gw.lda = p.ncp; gw.M = (int)V;
-    gw.B = xt + t0; gw.ldb = p.Np; gw.N = (int)H;
-    gw.K = (int)round_up(rows, kChunk);
-    gw.splits = 1; gw.k_per_split = (int)round_up(gw.K, kRowBytes / p.esz);
+    gw.A = ez; gw.lda = p.Vp; gw.M = (int)V;
+    gw.B = X + t0 * H; gw.ldb = H; gw.N = (int)H;
+    gw.K = rows;
+    gw.splits = 1; gw.k_per_split = (int)round_up(rows, kTileBytes / p.esz);
     gw.group_m = 4;
-    gw.out = dW; gw.ldo = H; gw.acc = acc; gw.ldacc = H;
-    gw.mode = p.chunks == 1 ? DW_ONLY : (c == 0 ? DW_FIRST : (c == p.chunks - 1 ? DW_LAST : DW_MID));
+    gw.out = dW; gw.ldo = H;
+    gw.mode = c == 0 ? DW_STORE : DW_ACCUMULATE;
     {
     KernelTimer t(T_DW, s);
-    if (launch_gemm<T, EPI_DW>(gw, s) != hipSuccess) return LCE_ERR_HIP;
+    if (launch_gemm<T, EPI_DW, true, true>(gw, s) != hipSuccess) return LCE_ERR_HIP;
     }
   }
 

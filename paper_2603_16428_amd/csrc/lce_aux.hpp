@@ -95,36 +95,31 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   }
 }
 
-// dlogits. For token i of the chunk and vocabulary id v (slice t = v / 128):
-//   dZ[i][v] = g_i exp(m_t,i - lse_i) e[i][v] - g_i [v == y_i],   g_i = valid_i / n_valid (mean) or valid_i.
-// e (token-major, pitch ldz) is overwritten with dZ; dZ^T (vocabulary-major, pitch ldt) is written
-// through an LDS transpose. Entries outside the valid tokens / vocabulary but inside the pitches
-// are written as zeros (the contractions read them as padding). Tile: 64 tokens x 128 ids.
+// dlogits, in place. For token i of the chunk and vocabulary id v (slice t = v / 128):
+//   dZ[i][v] = g_i exp(m_t,i - lse_i) e[i][v] - g_i [v == y_i],   g_i = valid_i / n_valid (mean) or valid_i,
+// where e = exp(z - m_t,i) was stored by the logits GEMM. Entries outside the valid tokens and
+// vocabulary but inside the pitches are written as zeros (the dH GEMM reads the vocabulary padding
+// of each row). One block per 64 tokens x 128 ids; 16-byte accesses.
 template <typename T>
-__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t ldz, T* __restrict__ zt,
-                                                      int64_t ldt, const float* __restrict__ pmax,
+__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t ldz, const float* __restrict__ pmax,
                                                       int64_t ldp, const float* __restrict__ lse,
                                                       const int64_t* __restrict__ y, int64_t ignore_index,
                                                       const int* __restrict__ n_valid, int mean, int rows,
                                                       int V) {
   constexpr int kVec = 16 / sizeof(T);          // elements per 16-byte access
-  constexpr int kTpr = 128 / kVec;              // threads per 128-id row
+  constexpr int kTpr = 128 / kVec;              // threads per 128-id row segment
   constexpr int kRowsPerPass = 256 / kTpr;
-  __shared__ T tile[64][128 + 8 / sizeof(T) * 2];
   const int v0 = blockIdx.x * 128, i0 = blockIdx.y * 64;
   const int slice = blockIdx.x;
   const int nv = *n_valid;
-  const float gscale = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
+  const float g = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
   const int tc = threadIdx.x % kTpr, tr = threadIdx.x / kTpr;
+  const int v = v0 + tc * kVec;
   for (int r = tr; r < 64; r += kRowsPerPass) {
     const int i = i0 + r;
-    const int v = v0 + tc * kVec;
+    const int64_t lab = i < rows ? y[i] : ignore_index;
     T outv[kVec];
-    bool valid_tok = i < rows;
-    int64_t lab = valid_tok ? y[i] : ignore_index;
-    const bool valid = valid_tok && lab != ignore_index;
-    if (valid) {
-      const float g = gscale;
+    if (i < rows && lab != ignore_index) {
       const float c = g * __expf(pmax[(size_t)slice * ldp + i] - lse[i]);
       T ev[kVec];
       *(uint4*)ev = *(const uint4*)(ez + (size_t)i * ldz + v);
@@ -138,40 +133,7 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
 #pragma unroll
       for (int e = 0; e < kVec; ++e) outv[e] = from_f32<T>(0.f);
     }
-    // Rows beyond the chunk are written as zeros too: they are padding of dZ^T's columns.
     *(uint4*)(ez + (size_t)i * ldz + v) = *(const uint4*)outv;
-#pragma unroll
-    for (int e = 0; e < kVec; ++e) tile[r][tc * kVec + e] = outv[e];
-  }
-  __syncthreads();
-  // Transposed write: row v of dZ^T gets 64 tokens = 64 * sizeof(T) bytes.
-  constexpr int kTprT = 64 / kVec;              // threads per dZ^T row segment
-  constexpr int kRowsPerPassT = 256 / kTprT;
-  const int tcT = threadIdx.x % kTprT, trT = threadIdx.x / kTprT;
-  for (int r = trT; r < 128; r += kRowsPerPassT) {
-    T outv[kVec];
-#pragma unroll
-    for (int e = 0; e < kVec; ++e) outv[e] = tile[tcT * kVec + e][r];
-    *(uint4*)(zt + (size_t)(v0 + r) * ldt + i0 + tcT * kVec) = *(const uint4*)outv;
-  }
-}
-
-// out[c][r] = in[r][c] for r < R, c < C; columns r in [R, Rp) of out are zero-filled.
-// in: [R, ldi], out: [C, ldo] with ldo >= Rp. Tile 64 x 64 through LDS.
-template <typename T>
-__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int64_t ldi, int64_t R, int64_t C,
-                                                        T* __restrict__ out, int64_t ldo, int64_t Rp) {
-  __shared__ T tile[64][64 + 1];
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int k = ty; k < 64; k += 4) {
-    const int64_t r = r0 + k, c = c0 + tx;
-    tile[k][tx] = (r < R && c < C) ? in[r * ldi + c] : from_f32<T>(0.f);
-  }
-  __syncthreads();
-  for (int k = ty; k < 64; k += 4) {
-    const int64_t c = c0 + k, r = r0 + tx;
-    if (c < C && r < Rp) out[c * ldo + r] = tile[tx][k];
   }
 }
 
@@ -214,11 +176,6 @@ __global__ __launch_bounds__(1024) void loss_reduce_kernel(const float* __restri
     }
     *loss = (float)r;
   }
-}
-
-__global__ void zero_kernel(float* __restrict__ p, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) p[i] = 0.f;
 }
 
 }  // namespace lce

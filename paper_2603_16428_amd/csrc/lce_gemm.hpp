@@ -1,27 +1,42 @@
 // MFMA GEMM core for the three contractions of the fused linear + cross-entropy step.
 //
-//   C[m, n] = sum_k A[m, k] * B[n, k]      A: [M, K] pitch lda, B: [N, K] pitch ldb (K contiguous)
+//   C[m, n] = sum_k A(m, k) * B(n, k)
+//
+// Each operand is stored either K-contiguous (element (m, k) at P[m * ld + k]) or MN-contiguous
+// (element (m, k) at P[k * ld + m]). The three contractions use:
+//   logits^T = W . X_c^T     A = W [V, H] K-contig,        B = X_c [n_c, H] K-contig
+//   dH_c     = dZ_c . W      A = dZ_c [n_c, V] K-contig,   B = W [V, H] MN-contig
+//   dW      += dZ_c^T . X_c  A = dZ_c [n_c, V] MN-contig,  B = X_c [n_c, H] MN-contig
+// so no operand is ever transposed in memory.
 //
 // One workgroup computes a 256 x 256 tile of C with four waves (2 x 2), each wave a 128 x 128
 // sub-tile held as 4 x 4 blocks of the 32x32 MFMA accumulator (256 fp32 per lane, in AGPRs). K
-// advances in tiles of one 128-byte cache line per row (64 bf16 or 32 fp32); eight lanes load one
-// line (16 bytes each). Every K-tile is requested about two K-tiles ahead of its MFMAs: a single
-// K-tile in flight per CU leaves the MFMAs waiting on this access pattern's load latency, and three
-// LDS stages of both operands (192 KB) do not fit. So operand A streams straight into a ring of
-// three LDS slots (buffer_load ... lds) while operand B is parked in one of two register buffers
-// (buffer_load_dwordx4) and written (ds_write_b128) into one of two LDS slots during the preceding
-// K-tile: 160 KB of LDS and 64 VGPRs. The buffer descriptors' range check turns rows beyond M/N,
-// and K-tiles past the end, into zeros. LDS rows are XOR-swizzled in
-// 16-byte units so that the fragment reads (ds_read_b128) are free of bank conflicts. Fragments
-// are double-buffered in registers: the reads for the next 32 bytes of K are in flight while the
-// MFMAs of the current ones run.
+// advances in K-tiles of 64 bf16 (32 fp32); an operand's K-tile is 32 KB of LDS either way:
+// 256 rows of 128 bytes (K-contig) or 64 (32) K-rows of 512 (1024) bytes (MN-contig). Global loads
+// are 16 bytes per lane and read whole 128-byte lines.
+//
+// Every K-tile is requested about two K-tiles ahead of its MFMAs: with a single K-tile in flight per
+// CU the MFMAs wait on this access pattern's load latency, and three LDS stages of both operands
+// (192 KB) do not fit in the 160 KB of LDS. So operand A streams straight into a ring of three LDS
+// slots (buffer_load ... lds) while operand B is parked in one of two register buffers
+// (buffer_load_dwordx4, 64 VGPRs) and written (ds_write_b128) into one of two LDS slots during the
+// preceding K-tile. Buffer descriptors turn rows beyond M/N (K-contig) or K-rows beyond the K
+// range (MN-contig, one descriptor per K-tile), and K-tiles past the end, into zeros.
+//
+// Fragments: for the 32x32x16 bf16 MFMA a lane supplies 8 consecutive K of one row/column.
+// K-contig tiles give them with one ds_read_b128; MN-contig bf16 tiles with two ds_read_b64_tr_b16
+// (each 16-lane group reads four K-rows of 16 columns and the LDS transposes them so that lane j
+// receives column j of the four rows); MN-contig fp32 tiles with four ds_read_b32. The 16-byte
+// slots of every LDS row are XOR-swizzled so that these reads are free of bank conflicts.
+// Fragments are double-buffered in registers: the reads for the next 32 bytes of K are in flight
+// while the MFMAs of the current ones run.
 //
 // The epilogue decides what the tile becomes:
 //   LSE_FWD / LSE_BWD : C = logits^T tile (rows = vocabulary, columns = tokens). Per token and per
 //                       128-row vocabulary slice: the maximum m and sum exp(z - m) (the vocabulary-
 //                       tiled online log-sum-exp); LSE_BWD also stores e = exp(z - m) token-major.
 //   STORE             : C written as the output dtype (or as fp32 split-K partials).
-//   DW                : C added into the fp32 dW accumulator (first / middle / last chunk).
+//   DW                : C written into dW (first chunk) or added to it (later chunks).
 // STORE and DW issue the MFMAs with the operands swapped, so each lane holds four consecutive
 // columns of C and writes them as one vector.
 #pragma once
@@ -37,63 +52,68 @@ typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kTile = 256;                       // BM = BN
-constexpr int kRowBytes = 128;                   // bytes of K per row per K-tile (one cache line)
-constexpr int kSlots = kRowBytes / 16;           // 16-byte chunks per row
-constexpr int kPairs = kSlots / 2;               // 32-byte K-pairs (one MFMA step) per K-tile
-constexpr int kOperandBytes = kTile * kRowBytes; // 32 KB: one operand's K-tile
+constexpr int kTileBytes = 128;                  // bytes of K per row of a K-contig K-tile
+constexpr int kOperandBytes = 32 * 1024;         // one operand's K-tile in LDS
 constexpr int kASlots = 3;                       // A: ring of K-tiles filled by LDS-DMA
 constexpr int kBSlots = 2;                       // B: LDS slots filled from registers
 constexpr int kBBase = kASlots * kOperandBytes;  // B slots follow the A ring
 constexpr int kGemmSmem = (kASlots + kBSlots) * kOperandBytes;  // 160 KB, all of a CU's LDS
-constexpr int kLoadsPerOperand = kSlots;         // 16-byte loads per lane per operand K-tile
+constexpr int kLoadsPerOperand = 8;              // 16-byte loads per lane per operand K-tile
 constexpr int kGemmThreads = 256;
 constexpr int kLseSlice = 128;                   // vocabulary rows per log-sum-exp partial
 constexpr uint32_t kOOB = 0x80000000u;           // a buffer offset beyond every range check
 constexpr float kLog2e = 1.4426950408889634f;
 
 enum Epilogue { EPI_LSE_FWD = 0, EPI_LSE_BWD = 1, EPI_STORE = 2, EPI_DW = 3 };
-enum DwMode { DW_FIRST = 0, DW_MID = 1, DW_LAST = 2, DW_ONLY = 3 };
+enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1 };
 
 struct GemmArgs {
   const void* A;
   const void* B;
   int64_t lda, ldb;   // pitches in elements
-  int M, N, K;        // K: elements, a multiple of 16 bytes' worth
+  int M, N, K;        // K-contig operands need K to be a multiple of 16 bytes' worth
   int tiles_m, tiles_n, splits, k_per_split;  // k_per_split: a multiple of the K-tile
   int group_m;        // tile rows per raster group
   // epilogue
   void* out;          // LSE_BWD: e (token-major, pitch ldo); STORE: output or fp32 partials; DW: dW
   int64_t ldo;
-  float* acc;         // DW: fp32 accumulator [M, ldacc]
-  int64_t ldacc;
   float* pmax;        // LSE: [slices, ldp]
   float* psum;
   int64_t ldp;
   int mode;           // DW: DwMode; STORE: 1 = fp32 split-K partials at out + split * M * ldo
 };
 
-// 16-byte slot of logical chunk c (0..7) of LDS row r is c ^ swz(r): conflict-free fragment reads
-// whether the LDS serves 8 or 16 lanes' 16-byte reads per cycle.
-__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+// K-contig tiles: logical 16-byte chunk c (0..7) of LDS row r sits in slot c ^ swz_k(r).
+__device__ __forceinline__ int swz_k(int r) { return (r ^ (r >> 3)) & 7; }
+// MN-contig bf16 tiles: logical 16-byte slot s (0..31) of K-row k sits in slot s ^ swz_mn(k).
+__device__ __forceinline__ int swz_mn(int k) { return ((k & 1) ? 4 : 0) ^ ((k & 2) ? 10 : 0) ^ ((k & 8) ? 16 : 0); }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
-__device__ __forceinline__ const void* uniform_ptr(const void* p) {
-  const uint64_t v = (uint64_t)p;
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, off, 0, 0, 0);
+}
+
+__device__ __forceinline__ i16x4 read_tr(const char* lds) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)lds);
+}
+
+__device__ __forceinline__ uint64_t uniform64(uint64_t v) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return (const void*)(((uint64_t)hi << 32) | lo);
+  return ((uint64_t)hi << 32) | lo;
 }
 
 // Tile coordinates of linear block `bid`. The dispatcher places block b on XCD b % 8, so blocks
@@ -141,13 +161,147 @@ __device__ __forceinline__ void store4(float* p, float a, float b, float c, floa
   f32x4 v = {a, b, c, d};
   *(f32x4*)p = v;
 }
+__device__ __forceinline__ f32x4 load4(const bf16* p) {
+  const bf16x4 v = *(const bf16x4*)p;
+  return (f32x4){(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+__device__ __forceinline__ f32x4 load4(const float* p) { return *(const f32x4*)p; }
 
-template <typename T, int EPI>
+// Loads and fragment reads of one operand (the tile's 256 rows/columns starting at mn0).
+template <typename T, bool MN>
+struct Operand {
+  static constexpr int kEsz = (int)sizeof(T);
+  static constexpr int kBK = kTileBytes / kEsz;       // K per K-tile
+  static constexpr int kMnRowBytes = kTile * kEsz;    // MN-contig: bytes per K-row
+
+  const char* base;   // element (mn0, 0)
+  int64_t ld;
+  int kb, ke;         // K range of this split
+  // Byte offset of load j within a K-tile = row_off + j * row_step + (slot_x ^ xor_j(j)): a lane
+  // term, a uniform term and a compile-time XOR. Two registers per lane instead of eight offsets.
+  uint32_t row_off, slot_x, row_step;
+  int frag[4];        // per 32-row block: this lane's LDS byte offset at K-pair 0
+  __amdgpu_buffer_rsrc_t rsrc_k;  // K-contig: one descriptor for the whole run
+
+  __device__ __forceinline__ void init(const void* p, int64_t ld_, int mn0, int rows, int kb_, int ke_,
+                                       int w, int lane, int wsub) {
+    ld = ld_;
+    kb = kb_;
+    ke = ke_;
+    if constexpr (!MN) {
+      base = (const char*)p + (size_t)mn0 * ld * kEsz;
+      rsrc_k = make_rsrc((const void*)uniform64((uint64_t)base),
+                         __builtin_amdgcn_readfirstlane((uint32_t)rows * (uint32_t)ld * kEsz));
+      // Load j of wave w covers LDS bytes [(8w + j) KB, +1 KB): lane l holds row
+      // r = 64w + 8j + l/8, slot l%8, which is logical chunk c = (l%8) ^ swz_k(r) of the row, and
+      // swz_k(r) = (l/8) ^ j. So the byte offset is (64w + l/8) ld + 8j ld + 16 (((l%8) ^ (l/8)) ^ j).
+      row_off = (uint32_t)(64 * w + (lane >> 3)) * (uint32_t)ld * kEsz;
+      row_step = 8u * (uint32_t)ld * kEsz;
+      slot_x = (uint32_t)(((lane & 7) ^ (lane >> 3)) << 4);
+      // Fragment of block i: row wsub + 32i + l%32, logical chunk 2p + l/32.
+#pragma unroll
+      for (int i = 0; i < 4; ++i) frag[i] = (wsub + 32 * i + (lane & 31)) * kTileBytes;
+    } else {
+      base = (const char*)p + (size_t)mn0 * kEsz;
+      if constexpr (kEsz == 2) {
+        // Load j of wave w: lane l holds K-row kr = 16w + 2j + l/32, slot l%32, which is logical
+        // slot (l%32) ^ swz_mn(kr), and swz_mn(kr) = 4 (l/32) ^ 10 (j&1) ^ 16 ((j>>2)&1).
+        row_off = (uint32_t)(16 * w + (lane >> 5)) * (uint32_t)ld * 2;
+        row_step = 2u * (uint32_t)ld * 2;
+        slot_x = (uint32_t)(((lane & 31) ^ (4 * (lane >> 5))) << 4);
+        // Transposed reads: 16-lane group g, lane i' = l%16 reads K-row 16p + 8(g/2) + 4s + i'/4
+        // at column wsub + 32i + 16(g%2) + 4(i'%4). The swizzle depends only on row bits 0, 1
+        // and 3, all fixed by the lane, so the address is this base plus (16p + 4s) * 512.
+        // Block i only flips address bits 6-7: its 16-byte slot is block 0's XOR 4i (the column's
+        // slot bits 2-3 come from 32i alone), so frag[i] = frag[0] ^ (i << 6).
+        const int g = lane >> 4, ip = lane & 15;
+        const int r0 = 8 * (g >> 1) + (ip >> 2);
+        const int col = wsub + 16 * (g & 1) + 4 * (ip & 3);
+        frag[0] = r0 * kMnRowBytes + (((col >> 3) ^ swz_mn(r0)) << 4) + 8 * ((col >> 2) & 1);
+      } else {
+        // fp32: load j of wave w: lane l holds K-row 8w + j, slot l; fragment reads are plain.
+        row_off = (uint32_t)(8 * w) * (uint32_t)ld * 4;
+        row_step = (uint32_t)ld * 4;
+        slot_x = (uint32_t)(lane * 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) frag[i] = (4 * (lane >> 5)) * kMnRowBytes + (wsub + 32 * i + (lane & 31)) * 4;
+      }
+    }
+  }
+
+  // The compile-time XOR part of load j's offset.
+  static __device__ __forceinline__ constexpr uint32_t xor_j(int j) {
+    if constexpr (!MN) return (uint32_t)(j << 4);
+    else if constexpr (kEsz == 2) return (uint32_t)((((j & 1) ? 10 : 0) ^ (((j >> 2) & 1) ? 16 : 0)) << 4);
+    else return 0u;
+  }
+
+  // Descriptor for K-tile t. MN-contig: its valid K-rows only, so that rows at or beyond ke,
+  // including whole K-tiles past the end, read zeros without touching memory.
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(int t) const {
+    if constexpr (!MN) {
+      return rsrc_k;
+    } else {
+      const int k0 = kb + t * kBK;
+      const int nrows = max(0, min(kBK, ke - k0));
+      const char* p = base + (size_t)(k0 < ke ? k0 : kb) * ld * kEsz;
+      return make_rsrc((const void*)uniform64((uint64_t)p),
+                       __builtin_amdgcn_readfirstlane((uint32_t)nrows * (uint32_t)ld * kEsz));
+    }
+  }
+
+  // Byte offset of load j of K-tile t (kOOB where a K-contig chunk lies at or beyond ke). The sum
+  // is formed where it is used: hoisted out of the main loop, the sixteen offsets of two operands
+  // would outgrow the registers and be spilled (and spill traffic would upset the vmcnt waits).
+  __device__ __forceinline__ uint32_t offset(int t, int j) const {
+    uint32_t o;
+    asm volatile("v_xor_b32 %0, %2, %1\n\tv_add3_u32 %0, %0, %3, %4"
+                 : "=&v"(o)
+                 : "v"(slot_x), "s"(xor_j(j)), "v"(row_off), "s"((uint32_t)j * row_step));
+    if constexpr (!MN) {
+      const int k0 = kb + t * kBK;
+      const int kc = (int)(((slot_x ^ xor_j(j)) >> 4) * (16 / kEsz));  // first K of the chunk
+      return k0 + kc < ke ? o + (uint32_t)k0 * kEsz : kOOB;
+    } else {
+      return o;
+    }
+  }
+
+  // Fragment of K-pair p of block i from the LDS tile at `st`.
+  __device__ __forceinline__ f32x4 fragment(const char* st, int p, int i, int khalf, int sw) const {
+    if constexpr (!MN) {
+      return *(const f32x4*)(st + frag[i] + (((2 * p + khalf) ^ sw) << 4));
+    } else if constexpr (kEsz == 2) {
+      // Issued as inline assembly: the compiler cannot tell which LDS bytes the transposing read
+      // builtin touches, and so would wait for every outstanding LDS-DMA load before it. The
+      // caller waits for these reads itself (see sync_frags). The address, (frag[0] ^ (i << 6)) +
+      // tile base, is formed here too: hoisted, the per-block addresses of two such operands would
+      // be spilled.
+      i16x4 lo, hi;
+      uint32_t a;
+      asm volatile(
+          "v_xor_b32 %2, %3, %4\n\t"
+          "v_add_u32 %2, %5, %2\n\t"
+          "ds_read_b64_tr_b16 %0, %2 offset:%6\n\t"
+          "ds_read_b64_tr_b16 %1, %2 offset:%7"
+          : "=v"(lo), "=v"(hi), "=&v"(a)
+          : "s"(i << 6), "v"(frag[0]), "s"((uint32_t)(uintptr_t)(lds_void*)st), "i"((16 * p) * kMnRowBytes),
+            "i"((16 * p + 4) * kMnRowBytes));
+      const i16x4 v[2] = {lo, hi};
+      return __builtin_bit_cast(f32x4, v);
+    } else {
+      const char* q = st + frag[i] + (8 * p) * kMnRowBytes;
+      return (f32x4){*(const float*)q, *(const float*)(q + kMnRowBytes), *(const float*)(q + 2 * kMnRowBytes),
+                     *(const float*)(q + 3 * kMnRowBytes)};
+    }
+  }
+};
+
+template <typename T, int EPI, bool A_MN, bool B_MN>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   constexpr int kEsz = (int)sizeof(T);
-  constexpr int kChunk = 16 / kEsz;        // elements per 16-byte chunk
-  constexpr int kBK = kRowBytes / kEsz;    // elements per K-tile
+  constexpr int kBK = kTileBytes / kEsz;   // elements per K-tile
   constexpr bool kSwap = (EPI == EPI_STORE || EPI == EPI_DW);
 
   const int lane = threadIdx.x & 63;
@@ -165,69 +319,39 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   const int kb = split * g.k_per_split;
   const int ke = min(g.K, kb + g.k_per_split);
 
-  const int rows_a = min(kTile, g.M - m0), rows_b = min(kTile, g.N - n0);
-  const __amdgpu_buffer_rsrc_t ra =
-      make_rsrc(uniform_ptr((const char*)g.A + (size_t)m0 * g.lda * kEsz),
-                __builtin_amdgcn_readfirstlane((uint32_t)rows_a * (uint32_t)g.lda * kEsz));
-  const __amdgpu_buffer_rsrc_t rb =
-      make_rsrc(uniform_ptr((const char*)g.B + (size_t)n0 * g.ldb * kEsz),
-                __builtin_amdgcn_readfirstlane((uint32_t)rows_b * (uint32_t)g.ldb * kEsz));
-
-  // Loader: load j of wave w covers LDS bytes [(8w + j) * 1 KB, +1 KB) of an operand K-tile; lane
-  // l holds row 8(8w + j) + l/8, 16-byte slot l%8, which is logical chunk (l%8) ^ swz(row) of the
-  // row. Each group of eight lanes reads one whole 128-byte line.
-  uint32_t off_a[kSlots], off_b[kSlots];
-  int kc[kSlots];
+  Operand<T, A_MN> opa;
+  Operand<T, B_MN> opb;
+  opa.init(g.A, g.lda, m0, min(kTile, g.M - m0), kb, ke, w, lane, wm * 128);
+  opb.init(g.B, g.ldb, n0, min(kTile, g.N - n0), kb, ke, w, lane, wn * 128);
+  const int khalf = lane >> 5;
+  // K-contig fragments: swz_k(row) depends on row % 64 only, the same for a lane's A and B rows.
+  int swi[4];
 #pragma unroll
-  for (int j = 0; j < kSlots; ++j) {
-    const int r = (w * kSlots + j) * (64 / kSlots) + lane / kSlots;
-    const int c = (lane % kSlots) ^ swz(r);
-    kc[j] = c * kChunk;
-    off_a[j] = (uint32_t)r * (uint32_t)g.lda * kEsz + (uint32_t)(c * 16);
-    off_b[j] = (uint32_t)r * (uint32_t)g.ldb * kEsz + (uint32_t)(c * 16);
-  }
+  for (int i = 0; i < 4; ++i) swi[i] = swz_k(i * 32 + (lane & 31));
 
-  // A K-tile t: LDS-DMA into ring slot t % 3. Chunks at or beyond ke, including whole K-tiles past
-  // the end, read zeros without touching memory, so every iteration issues the same number of
-  // loads and the wait counts below are constants.
+  // A K-tile t: LDS-DMA into ring slot t % 3.
   auto load_a = [&](int t) {
-    const int k0 = kb + t * kBK;
-    const uint32_t koff = (uint32_t)k0 * kEsz;
-    char* st = smem + (t % kASlots) * kOperandBytes + w * kSlots * 1024;
+    const __amdgpu_buffer_rsrc_t r = opa.rsrc(t);
+    char* st = smem + (t % kASlots) * kOperandBytes + w * 8 * 1024;
 #pragma unroll
-    for (int j = 0; j < kSlots; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(st + j * 1024), 16,
-                                               k0 + kc[j] < ke ? off_a[j] + koff : kOOB, 0, 0, 0);
+    for (int j = 0; j < 8; ++j) dma16(r, st + j * 1024, opa.offset(t, j));
   };
   // B K-tile t: into register buffer t % 2 (the caller passes that parity as a constant, so that
   // the buffers stay in registers) ...
-  u32x4 vb[2][kSlots];
+  u32x4 vb[2][8];
   auto load_b = [&](int t, auto par) {
-    const int k0 = kb + t * kBK;
-    const uint32_t koff = (uint32_t)k0 * kEsz;
+    const __amdgpu_buffer_rsrc_t r = opb.rsrc(t);
 #pragma unroll
-    for (int j = 0; j < kSlots; ++j) vb[par][j] = load16(rb, k0 + kc[j] < ke ? off_b[j] + koff : kOOB);
+    for (int j = 0; j < 8; ++j) vb[par][j] = load16(r, opb.offset(t, j));
   };
-  // ... then from there into LDS slot t % 2.
+  // ... then from there into LDS slot t % 2, at the same place LDS-DMA would have put it.
   auto write_b = [&](auto par) {
-    char* st = smem + kBBase + par * kOperandBytes + w * kSlots * 1024 + lane * 16;
+    char* st = smem + kBBase + par * kOperandBytes + w * 8 * 1024 + lane * 16;
 #pragma unroll
-    for (int j = 0; j < kSlots; ++j) *(u32x4*)(st + j * 1024) = vb[par][j];
+    for (int j = 0; j < 8; ++j) *(u32x4*)(st + j * 1024) = vb[par][j];
   };
   using P0 = std::integral_constant<int, 0>;
   using P1 = std::integral_constant<int, 1>;
-
-  // Fragment reads: block i covers rows wm*128 + 32i + (l%32) of A (wn*... of B); K-pair p reads
-  // logical chunk 2p + l/32 (lanes l and l+32 carry the two 16-byte halves of 32 bytes of K).
-  // swz(row) depends on row % 64 only: it is the same for a lane's A and B rows of block i.
-  int frag_a[4], frag_b[4], swi[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    frag_a[i] = (wm * 128 + i * 32 + (lane & 31)) * kRowBytes;
-    frag_b[i] = (wn * 128 + i * 32 + (lane & 31)) * kRowBytes;
-    swi[i] = swz(i * 32 + (lane & 31));
-  }
-  const int khalf = lane >> 5;
 
   f32x16 acc[4][4];
 #pragma unroll
@@ -240,11 +364,24 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   auto read_frags = [&](int t, int p, int buf) {
     const char* sa = smem + (t % kASlots) * kOperandBytes;
     const char* sb = smem + kBBase + (t & 1) * kOperandBytes;
-    const int c = 2 * p + khalf;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      fa[buf][i] = *(const f32x4*)(sa + frag_a[i] + ((c ^ swi[i]) << 4));
-      fb[buf][i] = *(const f32x4*)(sb + frag_b[i] + ((c ^ swi[i]) << 4));
+      fa[buf][i] = opa.fragment(sa, p, i, khalf, swi[i]);
+      fb[buf][i] = opb.fragment(sb, p, i, khalf, swi[i]);
+    }
+  };
+  // Fragment reads issued as inline assembly are invisible to the compiler's wait insertion: at
+  // the start of each section wait for all earlier LDS traffic (the previous section's reads, long
+  // since done), with the fragment registers as operands so that no MFMA moves above the wait.
+  auto sync_frags = [&]() {
+    if constexpr ((A_MN || B_MN) && kEsz == 2) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(fa[0][0]), "+v"(fa[0][1]), "+v"(fa[0][2]), "+v"(fa[0][3]), "+v"(fb[0][0]),
+                     "+v"(fb[0][1]), "+v"(fb[0][2]), "+v"(fb[0][3]), "+v"(fa[1][0]), "+v"(fa[1][1]),
+                     "+v"(fa[1][2]), "+v"(fa[1][3]), "+v"(fb[1][0]), "+v"(fb[1][1]), "+v"(fb[1][2]),
+                     "+v"(fb[1][3])
+                   :
+                   : "memory");
     }
   };
   auto mma = [&](int buf) {
@@ -268,40 +405,44 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   // loads outstanding". The scheduling-group hints pin the interleaving; fragment reads precede
   // LDS-bound loads in program order (the compiler keeps LDS reads before LDS writes that follow).
   constexpr int kAfter = 3 * kLoadsPerOperand;
-  auto sched = [](int n_ds_read, int n_ds_write, int n_vmem, bool vmem_first) {
+  constexpr int kReads = (A_MN ? 0 : 4) + (B_MN ? 0 : 4);  // compiler-visible LDS reads per K-pair
+  auto sched = [](int n_ds_write, int n_vmem) {
     if constexpr (kEsz != 2) return;  // fp32: four MFMAs per K-pair; left to the compiler
+    // The section's LDS reads go one after each of its first MFMAs.
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // one MFMA
-      if (i < n_ds_read) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-      if (i < n_ds_write) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS write
-      if (vmem_first ? i < n_vmem : i >= 16 - n_vmem)
-        __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);                     // one global load
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                  // one MFMA
+      if (i < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                 // one LDS read
+      if (i < n_ds_write) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);             // one LDS write
+      if (i >= 16 - n_vmem) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);           // one global load
     }
     __builtin_amdgcn_sched_barrier(0);  // each section is scheduled on its own
   };
   // One iteration for K-tile kt, whose parity is `par` (a constant).
   auto iteration = [&](int kt, auto par) {
     constexpr int q = decltype(par)::value ^ 1;
+    sync_frags();
     read_frags(kt, 1, 1);
     load_a(kt + 2);
     mma(0);
-    sched(8, 0, kLoadsPerOperand, false);
+    sched(0, kLoadsPerOperand);
+    sync_frags();
     read_frags(kt, 2, 0);
     mma(1);
-    sched(8, 0, 0, false);
+    sched(0, 0);
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kAfter) : "memory");  // B(kt + 1) landed
+    sync_frags();
     read_frags(kt, 3, 1);
     write_b(std::integral_constant<int, q>{});
     load_b(kt + 3, std::integral_constant<int, q>{});
     mma(0);
-    sched(8, kLoadsPerOperand, kLoadsPerOperand, false);
+    sched(kLoadsPerOperand, kLoadsPerOperand);
     // A(kt + 1) landed (vmcnt) for every wave (barrier); every wave wrote B(kt + 1) and finished
     // reading the slots that the next iteration refills (lgkmcnt before the barrier).
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAfter) : "memory");
     read_frags(kt + 1, 0, 0);
     mma(1);
-    sched(8, 0, 0, false);
+    sched(0, 0);
   };
   // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
   const int nk = (ke - kb + kBK - 1) / kBK;
@@ -408,39 +549,32 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
             }
         }
       } else {  // EPI_DW
-        float* a = g.acc + (size_t)row * g.ldacc;
         T* o = (T*)g.out + (size_t)row * g.ldo;
-        if (g.mode == DW_MID || g.mode == DW_LAST) {
-          // Load the whole row group first so that the loads are in flight together.
-          f32x4 prev[4][4];
+        if (g.mode == DW_ACCUMULATE) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              prev[j][q] = col < g.N ? *(const f32x4*)(a + col) : (f32x4){};
-            }
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
+          for (int j = 0; j < 4; ++j) {
+            // The four loads of a column block are in flight together.
+            f32x4 prev[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int col = nw + 32 * j + 8 * q + sub4;
-              if (col >= g.N) continue;
-              const float v0 = prev[j][q][0] + acc[i][j][4 * q], v1 = prev[j][q][1] + acc[i][j][4 * q + 1];
-              const float v2 = prev[j][q][2] + acc[i][j][4 * q + 2], v3 = prev[j][q][3] + acc[i][j][4 * q + 3];
-              if (g.mode == DW_MID) store4(a + col, v0, v1, v2, v3);
-              else store4(o + col, v0, v1, v2, v3);
+              prev[q] = col < g.N ? load4(o + col) : (f32x4){};
             }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int col = nw + 32 * j + 8 * q + sub4;
+              if (col < g.N)
+                store4(o + col, prev[q][0] + acc[i][j][4 * q], prev[q][1] + acc[i][j][4 * q + 1],
+                       prev[q][2] + acc[i][j][4 * q + 2], prev[q][3] + acc[i][j][4 * q + 3]);
+            }
+          }
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int col = nw + 32 * j + 8 * q + sub4;
-              if (col >= g.N) continue;
-              if (g.mode == DW_FIRST)
-                store4(a + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              else
+              if (col < g.N)
                 store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
             }
         }

@@ -16,7 +16,9 @@ import pytest
 
 from paper_2603_16428_amd import build as B
 
-GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li{e}EEEvNS_8GemmArgsE" for t in ("DF16b", "f") for e in range(4)]
+# (epilogue, A MN-contiguous, B MN-contiguous) of the four GEMMs: logits (forward / backward), dH, dW.
+VARIANTS = [(0, 0, 0), (1, 0, 0), (2, 0, 1), (3, 1, 1)]
+GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li{e}ELb{a}ELb{b}EEEvNS_8GemmArgsE" for t in ("DF16b", "f") for e, a, b in VARIANTS]
 
 
 @pytest.fixture(scope="module")
@@ -49,6 +51,87 @@ def test_gemm_main_loop_has_no_scratch_traffic(asm, name):
     dma = [l for l in loop if l.startswith("buffer_load") and l.endswith("lds")]
     vload = [l for l in loop if l.startswith("buffer_load") and not l.endswith("lds")]
     writes = [l for l in loop if l.startswith("ds_write")]
+    tr = [l for l in loop if l.startswith("ds_read_b64_tr_b16")]
     # Two K-tiles per loop trip: 2 x 64 MFMA steps (x4 for fp32's 32x32x2), 2 x 8 loads of each kind.
     assert len(mfma) == (128 if "DF16b" in name else 512), len(mfma)
     assert len(dma) == 16 and len(vload) == 16 and len(writes) == 16
+    # MN-contiguous bf16 operands: 2 transposing LDS reads per fragment x 4 fragments per K-pair x
+    # 4 K-pairs per K-tile x 2 K-tiles.
+    n_mn = name.count("ELb1")
+    assert len(tr) == (2 * 4 * 4 * 2 * n_mn if "DF16b" in name else 0), len(tr)
+
+
+# ---- LDS layout model: the index formulas of the GEMM loaders and fragment reads -------------
+# These restate, in Python, the per-lane formulas of gemm_kernel (Operand::init / offset /
+# fragment) and check that every fragment read finds the element the loader put there.
+
+def _swz_k(r):
+    return (r ^ (r >> 3)) & 7
+
+
+def _swz_mn(k):
+    return (4 if k & 1 else 0) ^ (10 if k & 2 else 0) ^ (16 if k & 8 else 0)
+
+
+def test_k_contiguous_layout_model():
+    ld = 1000  # any pitch (elements); bf16
+    stored = {}  # LDS byte -> (row, k) element index of its first bf16
+    for w in range(4):
+        for j in range(8):
+            for lane in range(64):
+                row_off = (64 * w + (lane >> 3)) * ld * 2
+                slot_x = ((lane & 7) ^ (lane >> 3)) << 4
+                off = row_off + j * 8 * ld * 2 + (slot_x ^ (j << 4))
+                row, kbyte = divmod(off, ld * 2)
+                lds = (8 * w + j) * 1024 + lane * 16
+                stored[lds] = (row, kbyte // 2)
+    for wsub in (0, 128):
+        for i in range(4):
+            for lane in range(64):
+                sw = _swz_k(i * 32 + (lane & 31))
+                for p in range(4):
+                    c = 2 * p + (lane >> 5)
+                    lds = (wsub + 32 * i + (lane & 31)) * 128 + ((c ^ sw) << 4)
+                    assert stored[lds] == (wsub + 32 * i + (lane & 31), 8 * c)
+
+
+def test_mn_contiguous_bf16_layout_model():
+    ld = 4096
+    stored = {}  # LDS byte -> (k-row, column) of its first bf16
+    for w in range(4):
+        for j in range(8):
+            for lane in range(64):
+                row_off = (16 * w + (lane >> 5)) * ld * 2
+                slot_x = ((lane & 31) ^ (4 * (lane >> 5))) << 4
+                xj = ((10 if j & 1 else 0) ^ (16 if (j >> 2) & 1 else 0)) << 4
+                off = row_off + j * 2 * ld * 2 + (slot_x ^ xj)
+                kr, cbyte = divmod(off, ld * 2)
+                lds = (8 * w + j) * 1024 + lane * 16
+                assert kr == 2 * (8 * w + j) + (lane >> 5)
+                for e in range(8):
+                    stored[lds + 2 * e] = (kr, cbyte // 2 + e)
+    conflicts = 0
+    for wsub in (0, 128):
+        g_ = [lane >> 4 for lane in range(64)]
+        for i in range(4):
+            for p in range(4):
+                for s in range(2):
+                    got, addrs = {}, []
+                    for lane in range(64):
+                        g, ip = lane >> 4, lane & 15
+                        r0 = 8 * (g >> 1) + (ip >> 2)
+                        col = wsub + 16 * (g & 1) + 4 * (ip & 3)
+                        frag0 = r0 * 512 + (((col >> 3) ^ _swz_mn(r0)) << 4) + 8 * ((col >> 2) & 1)
+                        a = (frag0 ^ (i << 6)) + (16 * p + 4 * s) * 512
+                        addrs.append(a)
+                        got[lane] = [stored[a + 2 * e] for e in range(4)]   # 4 consecutive columns
+                    for lane in range(64):   # the transposed delivery of ds_read_b64_tr_b16
+                        g, jj = lane >> 4, lane & 15
+                        recv = [got[16 * g + 4 * e + jj // 4][jj % 4] for e in range(4)]
+                        k0 = 16 * p + 8 * (lane >> 5) + 4 * s
+                        assert recv == [(k0 + e, wsub + 32 * i + (lane & 31)) for e in range(4)]
+                    for nb, grp in ((32, 16), (64, 32)):
+                        for g0 in range(0, 64, grp):
+                            banks = [((a // 4) + b) % nb for a in addrs[g0:g0 + grp] for b in (0, 1)]
+                            conflicts += len(banks) - len(set(banks))
+    assert conflicts == 0
