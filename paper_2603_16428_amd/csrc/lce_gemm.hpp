@@ -444,6 +444,32 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     mma(1);
     sched(0, 0);
   };
+  // bf16 dW accumulation (chunks after the first): the tile's current dW values are loaded here,
+  // raw, in flight together with the loads that fill the pipeline, and become the accumulators'
+  // starting values, so the epilogue only stores. (fp32 adds them in the epilogue instead: its
+  // 256 values per lane would not fit next to the pipeline's registers.)
+  const int mw = m0 + wm * 128, nw = n0 + wn * 128;
+  const int sub4 = 4 * (lane >> 5);
+  const int l32 = lane & 31;
+  constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
+  const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
+  bf16x4 prev[kPreload ? 4 : 1][4][4];
+  if constexpr (kPreload) {
+    if (accumulate) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = mw + 32 * i + l32;
+        const bf16* o = (const bf16*)g.out + (size_t)row * g.ldo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            prev[i][j][q] = (row < g.M && col < g.N) ? *(const bf16x4*)(o + col) : (bf16x4){};
+          }
+      }
+    }
+  }
   // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
   const int nk = (ke - kb + kBK - 1) / kBK;
   if (nk > 0) {
@@ -451,6 +477,18 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     load_a(0);
     load_b(1, P1{});
     load_a(1);
+    if constexpr (kPreload) {
+      if (accumulate) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] = (float)prev[i][j][q][e];
+      }
+    }
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsPerOperand) : "memory");  // B(0) landed
     write_b(P0{});
     load_b(2, P0{});
@@ -469,9 +507,6 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   // ---- epilogue. Without the swap, accumulator element r of block (i, j) sits at
   //      row = 32i + 8(r/4) + 4(l/32) + r%4, col = 32j + l%32 of the wave's 128 x 128 sub-tile;
   //      with it, at row = 32i + l%32, col = 32j + 8(r/4) + 4(l/32) + r%4.
-  const int mw = m0 + wm * 128, nw = n0 + wn * 128;
-  const int sub4 = 4 * (lane >> 5);
-  const int l32 = lane & 31;
 
   if constexpr (EPI == EPI_LSE_FWD || EPI == EPI_LSE_BWD) {
     if (mw >= g.M) return;
@@ -548,35 +583,23 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
                 store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
             }
         }
-      } else {  // EPI_DW
+      } else {  // EPI_DW (bf16: the accumulators already hold the earlier chunks' sum)
         T* o = (T*)g.out + (size_t)row * g.ldo;
-        if (g.mode == DW_ACCUMULATE) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            // The four loads of a column block are in flight together.
-            f32x4 prev[4];
+        for (int j = 0; j < 4; ++j) {
+          f32x4 base[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              prev[q] = col < g.N ? load4(o + col) : (f32x4){};
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              if (col < g.N)
-                store4(o + col, prev[q][0] + acc[i][j][4 * q], prev[q][1] + acc[i][j][4 * q + 1],
-                       prev[q][2] + acc[i][j][4 * q + 2], prev[q][3] + acc[i][j][4 * q + 3]);
-            }
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            base[q] = (!kPreload && accumulate && col < g.N) ? load4(o + col) : (f32x4){};
           }
-        } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              if (col < g.N)
-                store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-            }
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            if (col < g.N)
+              store4(o + col, base[q][0] + acc[i][j][4 * q], base[q][1] + acc[i][j][4 * q + 1],
+                     base[q][2] + acc[i][j][4 * q + 2], base[q][3] + acc[i][j][4 * q + 3]);
+          }
         }
       }
     }

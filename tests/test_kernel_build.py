@@ -33,13 +33,24 @@ def asm():
         return open(os.path.join(d, files[0])).read()
 
 
-def _main_loop(asm_text, name):
+def _main_loop(asm_text, name, with_prologue=False):
     start = asm_text.index(name + ":")
     end = asm_text.index(".Lfunc_end", start)
     body = asm_text[start:end].splitlines()
     lo = next(i for i, l in enumerate(body) if "Loop Header" in l)
     hi = next(i for i, l in enumerate(body) if i > lo and "s_cbranch" in l)
+    if with_prologue:
+        lo = 0
     return [l.strip() for l in body[lo:hi + 1] if l.strip() and not l.strip().startswith(";")]
+
+
+@pytest.mark.parametrize("name", GEMMS)
+def test_gemm_pipeline_fill_has_no_scratch_traffic(asm, name):
+    # The prologue's waits are hand-counted too: no spill traffic from the kernel's start to the
+    # end of the main loop.
+    code = _main_loop(asm, name, with_prologue=True)
+    scratch = [l for l in code if l.startswith("scratch_") or re.match(r"buffer_(load|store)\S*\s.*\boff\b", l)]
+    assert not scratch, scratch[:4]
 
 
 @pytest.mark.parametrize("name", GEMMS)
