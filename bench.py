@@ -11,8 +11,10 @@ and the float64 CPU oracle timed on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -23,6 +25,54 @@ PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
 PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 METRIC = "fused LCE fwd+bwd tokens/s and % bf16 MFMA peak (H=4096,V=128256,N=8192)"
+KERNEL_SOURCES = ("paper_2603_16428_amd/csrc/lce_gemm.hpp", "paper_2603_16428_amd/csrc/lce_aux.hpp",
+                  "paper_2603_16428_amd/csrc/lce_api.hip")
+
+
+def kernel_source_hash() -> str:
+    """Identifies the kernels a stored counter measurement belongs to."""
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, kind: str):
+    """HBM bytes per launch of `kind` from the stored FETCH_SIZE / WRITE_SIZE summary.
+
+    The summary (profiles/lce_hbm_traffic_<workload>.md) holds a JSON block written from two
+    rocprofv3 --pmc runs of this script, both counters already scaled by what they read for a
+    plain device copy of known size. Returns None when there is no summary or when the kernel
+    sources have changed since the counters were taken.
+    """
+    path = os.path.join(ROOT, "profiles", f"lce_hbm_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        m = re.search(r"```json\n(.*?)\n```", f.read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    k = rec.get("per_launch", {}).get(kind)
+    return None if k is None else int(k["fetch_bytes"] + k["write_bytes"])
+
+
+def copy_calibration(mib: int):
+    """Plain device-to-device copies of known size: the yardstick for the HBM byte counters."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 3 copies of {n} bytes")
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def log(*a):
@@ -83,6 +133,8 @@ def main():
     ap.add_argument("--cpu-sample-tokens", type=int, default=3072)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="also run plain copies of this many MiB (yardstick for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -94,6 +146,7 @@ def main():
     import workloads
 
     lce.load_library()
+    log(f"kernel sources {kernel_source_hash()}")
     t0 = time.time()
     d = workloads.make_inputs(args.workload, seed=0)
     N, H, V = d["N"], d["H"], d["V"]
@@ -145,9 +198,12 @@ def main():
     per_launch_flops = 2.0 * N * H * V * args.steps / dom_launches
     achieved = per_launch_flops / (dom_ms / dom_launches * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None, "kernel": dom,
+                "frac": round(achieved / peak, 4), "traffic": measured_traffic(args.workload, dom), "kernel": dom,
                 "per_launch_flops": per_launch_flops, "avg_launch_ms": dom_ms / dom_launches,
                 "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()}}
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
 
     memory = {"lce_peak_bytes": int(lce_peak)}
     if not args.no_memory:
