@@ -5,8 +5,9 @@
 One step = one lce_forward_backward call (loss, dH, dW) over the whole synthetic batch, inputs
 already resident in HBM. Prints ONE JSON line with tokens/s, the fraction of the bf16 dense MFMA
 peak (credited work 6*N*H*V), the live roofline of the dominant kernel (HIP events recorded by the
-library on its launch stream), peak device memory against a materialised-logits PyTorch baseline,
-and the float64 CPU oracle timed on a bounded sample of the same workload.
+library on its launch stream), the forward-only rate (loss without gradients, 2*N*H*V), peak
+device memory against a materialised-logits PyTorch baseline, and the float64 CPU oracle timed on
+a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -202,6 +203,24 @@ def main():
                 "per_launch_flops": per_launch_flops, "avg_launch_ms": dom_ms / dom_launches,
                 "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()}}
 
+    # Forward only (loss, no gradients): 2 N H V credited flops per call, reported beside the step.
+    fws = torch.empty(lce.workspace_size(N, H, V, dtype, False), dtype=torch.uint8, device=dev)
+    for _ in range(2):
+        lce.forward(X, W, y, d["ignore_index"], d["reduction"], workspace=fws)
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record(stream)
+    for _ in range(args.steps):
+        lce.forward(X, W, y, d["ignore_index"], d["reduction"], workspace=fws)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    fms = f0.elapsed_time(f1) / args.steps
+    del fws
+    forward_only = {"ms_per_call": round(fms, 4), "tokens_per_s": round(N / (fms * 1e-3), 1),
+                    "tflops": round(2.0 * N * H * V / (fms * 1e-3) / 1e12, 1),
+                    "mfma_peak_frac": round(2.0 * N * H * V / (fms * 1e-3) / 1e12 / peak, 4)}
+    log(f"forward only: {fms:.3f} ms/call")
+
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
 
@@ -221,7 +240,7 @@ def main():
         "data": "synthetic", "tflops": round(tflops, 1), "mfma_peak_frac": round(tflops / peak, 4),
         "config": {"workload": args.workload, "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
-        "roofline": roofline, "memory": memory,
+        "roofline": roofline, "forward_only": forward_only, "memory": memory,
     }
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host cores ...")

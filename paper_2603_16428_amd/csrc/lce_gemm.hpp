@@ -38,7 +38,8 @@
 //   STORE             : C written as the output dtype (or as fp32 split-K partials).
 //   DW                : C written into dW (first chunk) or added to it (later chunks).
 // STORE and DW issue the MFMAs with the operands swapped, so each lane holds four consecutive
-// columns of C and writes them as one vector.
+// columns of C (LSE_BWD: four consecutive vocabulary rows of e's token-major row). bf16 results
+// are regrouped between lanes l and l + 32 so that each store writes 32 contiguous bytes per row.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -54,6 +55,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -81,7 +83,8 @@ struct GemmArgs {
   int tiles_m, tiles_n, splits, k_per_split;  // k_per_split: a multiple of the K-tile
   int group_m;        // tile rows per raster group
   // epilogue
-  void* out;          // LSE_BWD: e (token-major, pitch ldo); STORE: output or fp32 partials; DW: dW
+  void* out;          // LSE_BWD: e (token-major, pitch ldo >= M rounded up to 128); STORE: output or
+                      // fp32 partials; DW: dW
   int64_t ldo;
   float* pmax;        // LSE: [slices, ldp]
   float* psum;
@@ -166,6 +169,37 @@ __device__ __forceinline__ f32x4 load4(const bf16* p) {
   return (f32x4){(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
 }
 __device__ __forceinline__ f32x4 load4(const float* p) { return *(const f32x4*)p; }
+
+// A bf16 output row segment of 32 elements held by lanes l and l + 32 (half = l / 32): lane l has
+// the 4-element groups at 8q + 4 half, q = 0..3, as v[4q + e]. One v_permlane32_swap per dword
+// regroups them so that lane l ends with elements 0-7 and 16-23 and lane l + 32 with 8-15 and
+// 24-31, and each store instruction writes 32 contiguous bytes of the row instead of 16 (the
+// stores of a tile's epilogue are a burst that every CU issues at about the same time).
+// in0 / in1: whether this lane's first / second 8 elements lie inside the output.
+__device__ __forceinline__ void store_row32(bf16* p, const f32x16& v, bool in0, bool in1) {
+  // The lane's half, recomputed here: kept alive from the prologue, the kernel would spill it.
+  uint32_t ln;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+  const int half = (int)(ln >> 5);
+  uint32_t a[4], b[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const bf16x4 x = {(bf16)v[4 * q], (bf16)v[4 * q + 1], (bf16)v[4 * q + 2], (bf16)v[4 * q + 3]};
+    const u32x2 u = __builtin_bit_cast(u32x2, x);
+    uint32_t* d = (q & 1) ? b : a;
+    d[(q >> 1) * 2] = u[0];
+    d[(q >> 1) * 2 + 1] = u[1];
+  }
+  // a = (q0, q2), b = (q1, q3); swap a's upper 32 lanes with b's lower 32 lanes.
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const auto r = __builtin_amdgcn_permlane32_swap(a[e], b[e], false, false);
+    a[e] = r[0];
+    b[e] = r[1];
+  }
+  if (in0) *(u32x4*)(p + 8 * half) = (u32x4){a[0], a[1], b[0], b[1]};
+  if (in1) *(u32x4*)(p + 16 + 8 * half) = (u32x4){a[2], a[3], b[2], b[3]};
+}
 
 // Loads and fragment reads of one operand (the tile's 256 rows/columns starting at mn0).
 template <typename T, bool MN>
@@ -492,8 +526,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsPerOperand) : "memory");  // B(0) landed
     write_b(P0{});
     load_b(2, P0{});
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(kAfter) : "memory");    // A(0) landed
-    __syncthreads();
+    // A(0) landed and B(0) written, for every wave. (Not __syncthreads: it would also wait for
+    // every load in flight.)
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAfter) : "memory");
     read_frags(0, 0, 0);
     for (int kt = 0; kt < nk; kt += 2) {
       iteration(kt, P0{});
@@ -538,15 +573,22 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
       if (col < g.N) {
         if constexpr (EPI == EPI_LSE_BWD) {
           T* e_row = (T*)g.out + (size_t)col * g.ldo;
+          if constexpr (kEsz == 2) {
+            // Whole 128-row wave slices: e's pitch is M rounded up to 128, and rows at or beyond M
+            // hold exp = 0 here.
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i) store_row32(e_row + mw + 32 * i, acc[i][j], true, true);
+          } else {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int row = mw + 32 * i + 8 * q + sub4;
-              if (row < g.M)
-                store4(e_row + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                       acc[i][j][4 * q + 3]);
-            }
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int row = mw + 32 * i + 8 * q + sub4;
+                if (row < g.M)
+                  store4(e_row + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                         acc[i][j][4 * q + 3]);
+              }
+          }
         }
         if (lane < 32) {
           g.pmax[(size_t)slice * g.ldp + col] = mx;
@@ -574,16 +616,32 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
             }
         } else {
           T* o = (T*)g.out + (size_t)row * g.ldo;
+          if constexpr (kEsz == 2) {
+            // N is a multiple of 8 for bf16, so an 8-column piece is all in or all out.
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              if (col < g.N)
-                store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+            for (int j = 0; j < 4; ++j) {
+              const int c0 = nw + 32 * j + 8 * (lane >> 5);
+              store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
             }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int col = nw + 32 * j + 8 * q + sub4;
+                if (col < g.N)
+                  store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+              }
+          }
         }
-      } else {  // EPI_DW (bf16: the accumulators already hold the earlier chunks' sum)
+      } else if constexpr (kPreload) {  // EPI_DW, bf16: the accumulators already hold the earlier chunks' sum
+        T* o = (T*)g.out + (size_t)row * g.ldo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c0 = nw + 32 * j + 8 * (lane >> 5);
+          store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
+        }
+      } else {  // EPI_DW, fp32
         T* o = (T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
