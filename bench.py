@@ -130,6 +130,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3_8b")
+    ap.add_argument("--dtype", choices=["bf16", "fp16", "fp32"], default=None,
+                    help="override the workload's element type (same draws, rounded to this type)")
     ap.add_argument("--chunk", type=int, default=0, help="tokens per chunk (0 = automatic)")
     ap.add_argument("--cpu-sample-tokens", type=int, default=3072)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -149,7 +151,7 @@ def main():
     lce.load_library()
     log(f"kernel sources {kernel_source_hash()}")
     t0 = time.time()
-    d = workloads.make_inputs(args.workload, seed=0)
+    d = workloads.make_inputs(args.workload, seed=0, dtype=args.dtype)
     N, H, V = d["N"], d["H"], d["V"]
     log(f"inputs {args.workload} N={N} H={H} V={V} ready in {time.time() - t0:.1f}s")
     dev = torch.device("cuda:0")
@@ -189,7 +191,7 @@ def main():
         + ", ".join(f"{k} {v[0] / args.steps:.3f} ms ({v[1]} launches)" for k, v in kern.items()))
 
     flops = 6.0 * N * H * V
-    peak = PEAK_BF16_TFLOPS if dtype == torch.bfloat16 else PEAK_FP32_TFLOPS
+    peak = PEAK_FP32_TFLOPS if dtype == torch.float32 else PEAK_BF16_TFLOPS  # fp16 dense = bf16 dense
     tflops = flops / (ms * 1e-3) / 1e12
     # Dominant kernel: the GEMM kind with the largest share of the step. Each of the three
     # contractions performs 2*N*H*V flops per step, spread over its launches.
@@ -236,9 +238,11 @@ def main():
     result = {
         "metric": METRIC, "value": round(N / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if dtype == torch.bfloat16 else "f32",
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": {torch.bfloat16: "bf16", torch.float16: "f16", torch.float32: "f32"}[dtype],
         "data": "synthetic", "tflops": round(tflops, 1), "mfma_peak_frac": round(tflops / peak, 4),
-        "config": {"workload": args.workload, "N": N, "H": H, "V": V, "reduction": d["reduction"],
+        "config": {"workload": args.workload if args.dtype is None else f"{args.workload}_{args.dtype}",
+                   "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
         "roofline": roofline, "forward_only": forward_only, "memory": memory,
     }

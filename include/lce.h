@@ -15,8 +15,9 @@
  * This is the paper's fused LinearCrossEntropy kernel (Section 3.3, "Integrated I/O and Compute
  * Co-Design", paragraph "Optimized Triton Kernels"): the projection is fused with the loss and the
  * gradients are produced chunk by chunk over the tokens, so that the N x V logits tensor is never
- * held in memory. The mixed-precision convention (bf16 tensors on the GPU, fp32 where precision
- * matters) follows Section 2.1 ("Static footprints") and Section 3.2.
+ * held in memory. The mixed-precision convention (bf16 or fp16 tensors on the GPU, fp32 where
+ * precision matters) follows Section 2.1 ("Static footprints") and Section 3.2 ("Optimized CPU
+ * Memory Layout with Shared Buffers": parameters and gradients in BF16/FP16 on the GPU).
  *
  * Conventions for every entry point
  *   - All tensor pointers are DEVICE pointers owned by the caller, row-major and contiguous:
@@ -30,12 +31,15 @@
  *   - Arguments are validated before anything is enqueued; on any error nothing is launched.
  *   - Results are deterministic: the same inputs on the same device give bitwise equal outputs
  *     (no atomics; every reduction has a fixed order).
- *   - Arithmetic: bf16 operands with fp32 accumulation (dtype BF16) or fp32 throughout (FP32).
- *     loss and lse are fp32; grad_hidden and grad_weight have the input dtype.
+ *   - Arithmetic: bf16 or fp16 operands with fp32 accumulation (dtype BF16, FP16) or fp32
+ *     throughout (FP32). loss and lse are fp32; grad_hidden and grad_weight have the input dtype.
+ *     With FP16 the library keeps its intermediate per-logit values in fp16 under fixed power-of-two
+ *     scales, so that the 1/n_valid-sized gradient entries do not underflow fp16's exponent range;
+ *     the results carry the precision of fp16 outputs.
  *   - A non-ignored label outside [0, V) is not an error the call can report (labels live on the
  *     device); its token's loss becomes NaN and it contributes no one-hot term to the gradients.
  *   - MEAN with no valid token gives loss 0 and zero gradients.
- *   - Supported shapes: N, H, V >= 1; H a multiple of 8 (BF16) or 4 (FP32); V * H and N * H
+ *   - Supported shapes: N, H, V >= 1; H a multiple of 8 (BF16, FP16) or 4 (FP32); V * H and N * H
  *     below 2^31 elements per 256-row slice limits (see LCE_ERR_UNSUPPORTED).
  */
 #ifndef LCE_H_
@@ -56,7 +60,7 @@ typedef enum {
   LCE_ERR_HIP = 4                  /* the HIP runtime reported an error while enqueueing      */
 } lce_status_t;
 
-typedef enum { LCE_DTYPE_FP32 = 0, LCE_DTYPE_BF16 = 1 } lce_dtype_t;
+typedef enum { LCE_DTYPE_FP32 = 0, LCE_DTYPE_BF16 = 1, LCE_DTYPE_FP16 = 2 } lce_dtype_t;
 
 /* Same order as torch's reduction enum. */
 typedef enum { LCE_REDUCTION_NONE = 0, LCE_REDUCTION_MEAN = 1, LCE_REDUCTION_SUM = 2 } lce_reduction_t;

@@ -105,14 +105,14 @@ int64_t auto_chunk(int64_t N, int64_t H) {
   return std::max<int64_t>(64, nc);
 }
 
-bool dtype_ok(int dtype) { return dtype == LCE_DTYPE_FP32 || dtype == LCE_DTYPE_BF16; }
+bool dtype_ok(int dtype) { return dtype == LCE_DTYPE_FP32 || dtype == LCE_DTYPE_BF16 || dtype == LCE_DTYPE_FP16; }
 
 // Fills `p`; returns LCE_OK or the status that the sizes deserve.
 lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward, int64_t chunk_tokens,
                        Plan& p, bool query_device) {
   if (N < 1 || H < 1 || V < 1 || !dtype_ok(dtype) || chunk_tokens < 0) return LCE_ERR_INVALID_ARGUMENT;
   p.N = N; p.H = H; p.V = V;
-  p.esz = dtype == LCE_DTYPE_BF16 ? 2 : 4;
+  p.esz = dtype == LCE_DTYPE_FP32 ? 4 : 2;
   p.backward = backward;
   if (H % (16 / p.esz) != 0) return LCE_ERR_UNSUPPORTED;
   int64_t nc = chunk_tokens == 0 ? auto_chunk(N, H) : chunk_tokens;
@@ -264,13 +264,14 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     } else {
       gh.out = dH + t0 * H; gh.ldo = H; gh.mode = 0;
     }
+    gh.n_valid = nvalid; gh.mean = mean;
     {
     KernelTimer t(T_DH, s);
     if (launch_gemm<T, EPI_STORE, false, true>(gh, s) != hipSuccess) return LCE_ERR_HIP;
     if (p.dh_splits > 1) {
       const int64_t count = (int64_t)rows * H;
       hipLaunchKernelGGL((split_reduce_kernel<T>), dim3((unsigned)cdiv(count / 4, 256)), dim3(256), 0, s, dhp,
-                         p.dh_splits, count, dH + t0 * H);
+                         p.dh_splits, count, dH + t0 * H, (const int*)nvalid, mean);
       if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
     }
     }
@@ -284,6 +285,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     gw.group_m = 4;
     gw.out = dW; gw.ldo = H;
     gw.mode = c == 0 ? DW_STORE : DW_ACCUMULATE;
+    gw.n_valid = nvalid; gw.mean = mean;
     {
     KernelTimer t(T_DW, s);
     if (launch_gemm<T, EPI_DW, true, true>(gw, s) != hipSuccess) return LCE_ERR_HIP;
@@ -328,6 +330,9 @@ lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* 
   if (dtype == LCE_DTYPE_BF16)
     return lce::run<lce::bf16>(p, (const lce::bf16*)hidden, (const lce::bf16*)weight, labels, ignore_index,
                                reduction, loss, lse, nullptr, nullptr, (char*)workspace, s);
+  if (dtype == LCE_DTYPE_FP16)
+    return lce::run<lce::f16>(p, (const lce::f16*)hidden, (const lce::f16*)weight, labels, ignore_index,
+                              reduction, loss, lse, nullptr, nullptr, (char*)workspace, s);
   return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss, lse,
                          nullptr, nullptr, (char*)workspace, s);
 }
@@ -347,6 +352,10 @@ lce_status_t lce_forward_backward(const void* hidden, const void* weight, const 
     return lce::run<lce::bf16>(p, (const lce::bf16*)hidden, (const lce::bf16*)weight, labels, ignore_index,
                                reduction, loss, nullptr, (lce::bf16*)grad_hidden, (lce::bf16*)grad_weight,
                                (char*)workspace, s);
+  if (dtype == LCE_DTYPE_FP16)
+    return lce::run<lce::f16>(p, (const lce::f16*)hidden, (const lce::f16*)weight, labels, ignore_index,
+                              reduction, loss, nullptr, (lce::f16*)grad_hidden, (lce::f16*)grad_weight,
+                              (char*)workspace, s);
   return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss,
                          nullptr, (float*)grad_hidden, (float*)grad_weight, (char*)workspace, s);
 }

@@ -8,9 +8,11 @@
 namespace lce {
 
 __device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+__device__ __forceinline__ float to_f32(f16 v) { return (float)v; }
 __device__ __forceinline__ float to_f32(float v) { return v; }
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+template <> __device__ __forceinline__ f16 from_f32<f16>(float v) { return (f16)v; }
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
 // n_valid = number of labels different from ignore_index, over all N tokens (the mean's divisor
@@ -99,7 +101,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 //   dZ[i][v] = g_i exp(m_t,i - lse_i) e[i][v] - g_i [v == y_i],   g_i = valid_i / n_valid (mean) or valid_i,
 // where e = exp(z - m_t,i) was stored by the logits GEMM. Entries outside the valid tokens and
 // vocabulary but inside the pitches are written as zeros (the dH GEMM reads the vocabulary padding
-// of each row). One block per 64 tokens x 128 ids; 16-byte accesses.
+// of each row). One block per 64 tokens x 128 ids; 16-byte accesses. For fp16 both e and dZ carry
+// the storage scales of Storage<f16> (dZ = (p - onehot) kDz for valid tokens; g is applied later).
 template <typename T>
 __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t ldz, const float* __restrict__ pmax,
                                                       int64_t ldp, const float* __restrict__ lse,
@@ -112,7 +115,8 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
   const int v0 = blockIdx.x * 128, i0 = blockIdx.y * 64;
   const int slice = blockIdx.x;
   const int nv = *n_valid;
-  const float g = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
+  const float g = Storage<T>::kDzUnscaled ? Storage<T>::kDz : (mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f);
+  constexpr float kInvE = 1.f / Storage<T>::kE;
   const int tc = threadIdx.x % kTpr, tr = threadIdx.x / kTpr;
   const int v = v0 + tc * kVec;
   for (int r = tr; r < 64; r += kRowsPerPass) {
@@ -120,7 +124,7 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
     const int64_t lab = i < rows ? y[i] : ignore_index;
     T outv[kVec];
     if (i < rows && lab != ignore_index) {
-      const float c = g * __expf(pmax[(size_t)slice * ldp + i] - lse[i]);
+      const float c = g * kInvE * __expf(pmax[(size_t)slice * ldp + i] - lse[i]);
       T ev[kVec];
       *(uint4*)ev = *(const uint4*)(ez + (size_t)i * ldz + v);
 #pragma unroll
@@ -137,16 +141,22 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
   }
 }
 
-// out[i][h] = sum_s part[s][i][h] (fixed order), converted to the output type.
+// out[i][h] = sum_s part[s][i][h] (fixed order), times the dz storage scale's inverse (1 unless
+// dz is stored unscaled), converted to the output type.
 template <typename T>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int splits,
-                                                           int64_t count, T* __restrict__ out) {
+                                                           int64_t count, T* __restrict__ out,
+                                                           const int* __restrict__ n_valid, int mean) {
   const int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (idx >= count) return;
   float4 s = *(const float4*)(part + idx);
   for (int k = 1; k < splits; ++k) {
     const float4 v = *(const float4*)(part + (size_t)k * count + idx);
     s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  if constexpr (Storage<T>::kDzUnscaled) {
+    const float sc = dz_epilogue_scale<T>(n_valid, mean);
+    s.x *= sc; s.y *= sc; s.z *= sc; s.w *= sc;
   }
   out[idx] = from_f32<T>(s.x);
   out[idx + 1] = from_f32<T>(s.y);

@@ -51,6 +51,9 @@ namespace lce {
 typedef __bf16 bf16;
 typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16;
+typedef f16 f16x8 __attribute__((ext_vector_type(8)));
+typedef f16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -90,6 +93,8 @@ struct GemmArgs {
   float* psum;
   int64_t ldp;
   int mode;           // DW: DwMode; STORE: 1 = fp32 split-K partials at out + split * M * ldo
+  const int* n_valid; // STORE (mode 0) / DW of 16-bit types whose dz is stored unscaled: the
+  int mean;           // valid-token count and reduction that give g (see Storage)
 };
 
 // K-contig tiles: logical 16-byte chunk c (0..7) of LDS row r sits in slot c ^ swz_k(r).
@@ -148,6 +153,11 @@ __device__ __forceinline__ void mfma_pair<bf16>(f32x16& c, const f32x4& a, const
 }
 
 template <>
+__device__ __forceinline__ void mfma_pair<f16>(f32x16& c, const f32x4& a, const f32x4& b) {
+  c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+template <>
 __device__ __forceinline__ void mfma_pair<float>(f32x16& c, const f32x4& a, const f32x4& b) {
   // 8 fp32 of K: each 32x32x2 step takes element s of both lanes' 4-vectors.
   c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], c, 0, 0, 0);
@@ -160,6 +170,10 @@ __device__ __forceinline__ void store4(bf16* p, float a, float b, float c, float
   bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
   *(bf16x4*)p = v;
 }
+__device__ __forceinline__ void store4(f16* p, float a, float b, float c, float d) {
+  f16x4 v = {(f16)a, (f16)b, (f16)c, (f16)d};
+  *(f16x4*)p = v;
+}
 __device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
   f32x4 v = {a, b, c, d};
   *(f32x4*)p = v;
@@ -168,15 +182,51 @@ __device__ __forceinline__ f32x4 load4(const bf16* p) {
   const bf16x4 v = *(const bf16x4*)p;
   return (f32x4){(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
 }
+__device__ __forceinline__ f32x4 load4(const f16* p) {
+  const f16x4 v = *(const f16x4*)p;
+  return (f32x4){(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
 __device__ __forceinline__ f32x4 load4(const float* p) { return *(const f32x4*)p; }
 
-// A bf16 output row segment of 32 elements held by lanes l and l + 32 (half = l / 32): lane l has
+// Storage scales of the 16-bit types. fp16 has a 5-bit exponent: with the mean's 1/n_valid the
+// gradient entries of a large vocabulary (~1e-9) would flush to zero, so for fp16 e is stored as
+// exp(z - m) 2^15 and dz as (p - [v == y]) 2^10, and the dH / dW epilogues apply
+// g 2^-10 (g = 1/n_valid for the mean, 1 for the sum). bf16 (fp32's exponent range) and fp32
+// store e and dz = g (p - [v == y]) as they are.
+template <typename T>
+struct Storage {
+  static constexpr float kE = 1.f;           // e is stored times kE
+  static constexpr bool kDzUnscaled = false;  // dz holds (p - onehot) kDz instead of g (p - onehot)
+  static constexpr float kDz = 1.f;
+};
+template <>
+struct Storage<f16> {
+  static constexpr float kE = 32768.f;
+  static constexpr bool kDzUnscaled = true;
+  static constexpr float kDz = 1024.f;
+};
+
+// The factor the dH / dW epilogues apply to their accumulators (1 unless dz is stored unscaled).
+template <typename T>
+__device__ __forceinline__ float dz_epilogue_scale(const int* n_valid, int mean) {
+  if constexpr (!Storage<T>::kDzUnscaled) {
+    return 1.f;
+  } else {
+    const int nv = *n_valid;
+    const float g = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
+    return g * (1.f / Storage<T>::kDz);
+  }
+}
+
+// A 16-bit output row segment of 32 elements held by lanes l and l + 32 (half = l / 32): lane l has
 // the 4-element groups at 8q + 4 half, q = 0..3, as v[4q + e]. One v_permlane32_swap per dword
 // regroups them so that lane l ends with elements 0-7 and 16-23 and lane l + 32 with 8-15 and
 // 24-31, and each store instruction writes 32 contiguous bytes of the row instead of 16 (the
 // stores of a tile's epilogue are a burst that every CU issues at about the same time).
 // in0 / in1: whether this lane's first / second 8 elements lie inside the output.
-__device__ __forceinline__ void store_row32(bf16* p, const f32x16& v, bool in0, bool in1) {
+template <typename T>
+__device__ __forceinline__ void store_row32(T* p, const f32x16& v, bool in0, bool in1) {
+  typedef T t4 __attribute__((ext_vector_type(4)));
   // The lane's half, recomputed here: kept alive from the prologue, the kernel would spill it.
   uint32_t ln;
   asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
@@ -184,7 +234,7 @@ __device__ __forceinline__ void store_row32(bf16* p, const f32x16& v, bool in0, 
   uint32_t a[4], b[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const bf16x4 x = {(bf16)v[4 * q], (bf16)v[4 * q + 1], (bf16)v[4 * q + 2], (bf16)v[4 * q + 3]};
+    const t4 x = {(T)v[4 * q], (T)v[4 * q + 1], (T)v[4 * q + 2], (T)v[4 * q + 3]};
     const u32x2 u = __builtin_bit_cast(u32x2, x);
     uint32_t* d = (q & 1) ? b : a;
     d[(q >> 1) * 2] = u[0];
@@ -485,7 +535,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   const int mw = m0 + wm * 128, nw = n0 + wn * 128;
   const int sub4 = 4 * (lane >> 5);
   const int l32 = lane & 31;
-  constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
+  constexpr bool kPreload = EPI == EPI_DW && std::is_same<T, bf16>::value;
   const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
   bf16x4 prev[kPreload ? 4 : 1][4][4];
   if constexpr (kPreload) {
@@ -567,7 +617,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
           const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
           const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
           s += e;
-          acc[i][j][r] = e;
+          acc[i][j][r] = e * Storage<T>::kE;
         }
       s += __shfl_xor(s, 32);
       if (col < g.N) {
@@ -599,6 +649,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   } else {
     // Swapped layout: lane owns rows mw + 32i + l%32 and 4 consecutive columns per (j, q).
     // N (the output pitch) is a multiple of 4 here, so a 4-column group is all in or all out.
+    const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = mw + 32 * i + l32;
@@ -617,9 +668,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
         } else {
           T* o = (T*)g.out + (size_t)row * g.ldo;
           if constexpr (kEsz == 2) {
-            // N is a multiple of 8 for bf16, so an 8-column piece is all in or all out.
+            // N is a multiple of 8 for 16-bit types, so an 8-column piece is all in or all out.
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
+              if constexpr (Storage<T>::kDzUnscaled) acc[i][j] *= sc;
               const int c0 = nw + 32 * j + 8 * (lane >> 5);
               store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
             }
@@ -641,7 +693,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
           const int c0 = nw + 32 * j + 8 * (lane >> 5);
           store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
         }
-      } else {  // EPI_DW, fp32
+      } else {  // EPI_DW, fp32 and fp16: add the earlier chunks' sum here
         T* o = (T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -655,8 +707,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
           for (int q = 0; q < 4; ++q) {
             const int col = nw + 32 * j + 8 * q + sub4;
             if (col < g.N)
-              store4(o + col, base[q][0] + acc[i][j][4 * q], base[q][1] + acc[i][j][4 * q + 1],
-                     base[q][2] + acc[i][j][4 * q + 2], base[q][3] + acc[i][j][4 * q + 3]);
+              store4(o + col, base[q][0] + sc * acc[i][j][4 * q], base[q][1] + sc * acc[i][j][4 * q + 1],
+                     base[q][2] + sc * acc[i][j][4 * q + 2], base[q][3] + sc * acc[i][j][4 * q + 3]);
           }
         }
       }

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "liblce.so")
 LCE_OK = 0
 STATUS = {0: "LCE_OK", 1: "LCE_ERR_INVALID_ARGUMENT", 2: "LCE_ERR_UNSUPPORTED",
           3: "LCE_ERR_WORKSPACE_TOO_SMALL", 4: "LCE_ERR_HIP"}
-DTYPES = {torch.float32: 0, torch.bfloat16: 1}
+DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
 EXPORTED = ("lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
             "lce_timing_enable", "lce_timing_read", "lce_status_string")
@@ -89,7 +89,7 @@ def _check_inputs(hidden, weight, labels):
     if hidden.dim() != 2 or weight.dim() != 2 or labels.dim() != 1:
         raise ValueError("expected hidden [N,H], weight [V,H], labels [N]")
     if hidden.dtype != weight.dtype or hidden.dtype not in DTYPES:
-        raise ValueError("hidden and weight must both be bfloat16 or both float32")
+        raise ValueError("hidden and weight must have the same dtype, one of bfloat16, float16, float32")
     if labels.dtype != torch.int64:
         raise ValueError("labels must be int64")
     N, H = hidden.shape

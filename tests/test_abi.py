@@ -11,7 +11,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "lce.h")
 
 OK, INVALID, UNSUPPORTED, WS_SMALL, HIP = 0, 1, 2, 3, 4
-BF16, FP32 = 1, 0
+BF16, FP32, FP16 = 1, 0, 2
 NONE, MEAN, SUM = 0, 1, 2
 FAKE = ctypes.c_void_p(0x1000)  # non-null, never dereferenced: every call below fails validation
 
@@ -55,7 +55,9 @@ def test_workspace_size(lib):
     assert ws(8, 8, 0, BF16, 1, 0) == 0
     assert ws(8, 8, 8, 7, 1, 0) == 0
     assert ws(8, 12, 8, BF16, 1, 0) == 0          # H not a multiple of 8 for bf16
+    assert ws(8, 12, 8, FP16, 1, 0) == 0          # nor for fp16
     assert ws(8, 12, 8, FP32, 1, 0) > 0           # fine for fp32
+    assert ws(8, 16, 8, FP16, 1, 0) == ws(8, 16, 8, BF16, 1, 0) > 0  # same 2-byte layout
     assert ws(300, 64, 100, BF16, 1, 100) == 0    # chunk must be a multiple of 64 when < N
     fwd = ws(8192, 4096, 128256, BF16, 0, 0)
     bwd = ws(8192, 4096, 128256, BF16, 1, 0)
@@ -91,7 +93,8 @@ def _fb(lib, **kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(hidden=None), INVALID), (dict(weight=None), INVALID), (dict(labels=None), INVALID),
     (dict(loss=None), INVALID), (dict(N=0), INVALID), (dict(H=-1), INVALID), (dict(V=0), INVALID),
-    (dict(dtype=5), INVALID), (dict(red=3), INVALID), (dict(H=60), UNSUPPORTED),
+    (dict(dtype=5), INVALID), (dict(dtype=3), INVALID), (dict(red=3), INVALID), (dict(H=60), UNSUPPORTED),
+    (dict(dtype=FP16, H=60), UNSUPPORTED),
     (dict(ws=None), WS_SMALL), (dict(wsb=16), WS_SMALL),
 ])
 def test_forward_validation(lib, kw, status):

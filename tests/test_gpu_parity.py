@@ -1,7 +1,8 @@
 """Parity of the HIP path (through the C ABI) with the float64 oracle, on the same seeded inputs.
 
 Tolerances: loss relative error <= 1e-3 and max|dH - ref|, max|dW - ref| <= 2e-2 * max|ref| for
-bf16 operands with fp32 accumulation; 1e-5 for the fp32 path.
+bf16 operands with fp32 accumulation; 1e-5 for the fp32 path; for fp16 (unit roundoff 2^-11, eight
+times finer than bf16's) 1e-3 and 5e-3 * max|ref|, the same margin of about ten unit roundoffs.
 
 Small cases run the whole oracle (several tiles, ragged tails, several chunks, split-K). The
 full-size workloads compare the loss and every token's log-sum-exp with values the oracle wrote
@@ -22,7 +23,7 @@ import workloads
 pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-TOL = {"bf16": (1e-3, 2e-2), "fp32": (1e-5, 1e-5)}
+TOL = {"bf16": (1e-3, 2e-2), "fp16": (1e-3, 5e-3), "fp32": (1e-5, 1e-5)}
 
 
 @pytest.fixture(scope="module")
@@ -87,6 +88,10 @@ RAGGED = [
     (37, 72, 1000, "fp32", 0),
     (300, 132, 2049, "fp32", 64),
     (260, 4, 129, "fp32", 0),
+    (37, 72, 1000, "fp16", 0),
+    (300, 136, 4099, "fp16", 64),
+    (513, 264, 2050, "fp16", 128),
+    (64, 1024, 33000, "fp16", 0),
 ]
 
 
@@ -100,6 +105,28 @@ def test_ragged_shapes(lce, N, H, V, dtype, chunk):
 def test_reductions(lce, reduction):
     d = workloads.random_case(200, 96, 3001, seed=3, w_std=0.3)
     _check_full(lce, d, reduction=reduction, chunk_tokens=64)
+
+
+@pytest.mark.parametrize("reduction", ["mean", "sum"])
+def test_fp16_large_vocabulary(lce, reduction):
+    # Llama-like inputs at a size the oracle finishes in seconds. With the mean, g p is ~3e-8 here,
+    # below fp16's smallest subnormal: this is the case the fp16 storage scales exist for.
+    d = workloads.make_inputs("llama3_8b", seed=1, N=1024, H=1024, V=32768, dtype="fp16")
+    _check_full(lce, d, reduction=reduction, chunk_tokens=256)
+
+
+def test_fp16_edge_cases(lce):
+    d = workloads.random_case(70, 32, 500, dtype="fp16", seed=5, ignore_frac=1.0)
+    loss, dH, dW = _check_full(lce, d)
+    assert loss.item() == 0.0 and torch.all(dH == 0) and torch.all(dW == 0)
+    d = workloads.random_case(100, 64, 3000, dtype="fp16", seed=8)
+    d["weight"] = torch.zeros_like(d["weight"])
+    X, W, y = _to_dev(d)
+    loss, dH, dW = lce.forward_backward(X, W, y)
+    assert abs(loss.item() - np.log(3000)) <= 1e-6 * np.log(3000)
+    assert torch.all(dH == 0)
+    tl, lse = lce.forward(X, W, y, reduction="none", return_lse=True)
+    assert torch.allclose(lse, torch.full_like(lse, float(np.log(3000))), rtol=1e-6)
 
 
 def test_vocab_of_one_and_two(lce):

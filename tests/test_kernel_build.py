@@ -18,7 +18,9 @@ from paper_2603_16428_amd import build as B
 
 # (epilogue, A MN-contiguous, B MN-contiguous) of the four GEMMs: logits (forward / backward), dH, dW.
 VARIANTS = [(0, 0, 0), (1, 0, 0), (2, 0, 1), (3, 1, 1)]
-GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li{e}ELb{a}ELb{b}EEEvNS_8GemmArgsE" for t in ("DF16b", "f") for e, a, b in VARIANTS]
+# Element types: bf16 (DF16b), fp16 (DF16_), fp32 (f).
+GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li{e}ELb{a}ELb{b}EEEvNS_8GemmArgsE"
+         for t in ("DF16b", "DF16_", "f") for e, a, b in VARIANTS]
 
 
 @pytest.fixture(scope="module")
@@ -64,12 +66,12 @@ def test_gemm_main_loop_has_no_scratch_traffic(asm, name):
     writes = [l for l in loop if l.startswith("ds_write")]
     tr = [l for l in loop if l.startswith("ds_read_b64_tr_b16")]
     # Two K-tiles per loop trip: 2 x 64 MFMA steps (x4 for fp32's 32x32x2), 2 x 8 loads of each kind.
-    assert len(mfma) == (128 if "DF16b" in name else 512), len(mfma)
+    assert len(mfma) == (128 if "DF16" in name else 512), len(mfma)
     assert len(dma) == 16 and len(vload) == 16 and len(writes) == 16
-    # MN-contiguous bf16 operands: 2 transposing LDS reads per fragment x 4 fragments per K-pair x
+    # MN-contiguous 16-bit operands: 2 transposing LDS reads per fragment x 4 fragments per K-pair x
     # 4 K-pairs per K-tile x 2 K-tiles.
     n_mn = name.count("ELb1")
-    assert len(tr) == (2 * 4 * 4 * 2 * n_mn if "DF16b" in name else 0), len(tr)
+    assert len(tr) == (2 * 4 * 4 * 2 * n_mn if "DF16" in name else 0), len(tr)
 
 
 # ---- LDS layout model: the index formulas of the GEMM loaders and fragment reads -------------

@@ -14,7 +14,7 @@ Recipe (identical on every machine with the same numpy and torch):
 * ``numpy.random.SeedSequence(seed).spawn(4)`` gives four independent PCG64
   streams, used for hidden, weight, labels and the ignore mask, in that order.
 * Values are drawn in float64, shaped and normalised in float64, then rounded
-  to the workload dtype by torch's float64 -> bfloat16 (or float32) conversion
+  to the workload dtype by torch's float64 -> bfloat16 (or float16, float32) conversion
   (round to nearest even).
 * "unit-RMS rows": each hidden row is g / sqrt(mean(g**2)) with g ~ N(0, 1),
   the shape of a post-RMSNorm activation.
@@ -34,6 +34,7 @@ import numpy as np
 import torch
 
 IGNORE_INDEX = -100
+TORCH_DTYPES = {"bf16": torch.bfloat16, "fp16": torch.float16, "fp32": torch.float32}
 
 # Rows of W are drawn in blocks of this many rows so that the float64 staging
 # buffer stays small; numpy's normal stream is sequential, so the values do not
@@ -47,7 +48,7 @@ class Workload:
     N: int            # tokens (batch x sequence)
     H: int            # hidden size
     V: int            # vocabulary size
-    dtype: str        # "bf16" or "fp32"
+    dtype: str        # "bf16", "fp16" or "fp32"
     hidden: str       # "normal", "normal_4_over_sqrt_h", "unit_rms"
     w_std: float
     labels: str       # "uniform" or "zipf"
@@ -59,7 +60,7 @@ class Workload:
 
     @property
     def torch_dtype(self):
-        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+        return TORCH_DTYPES[self.dtype]
 
 
 WORKLOADS = {
@@ -128,14 +129,17 @@ def _ignore_mask(rng, w: Workload, N: int) -> np.ndarray:
 
 
 def make_inputs(name: str, seed: int = 0, N: int | None = None, H: int | None = None,
-                V: int | None = None):
+                V: int | None = None, dtype: str | None = None):
     """Draw (hidden, weight, labels) for workload ``name`` as CPU torch tensors.
 
     ``N``/``H``/``V`` override the workload's sizes (same distributions), which
-    the tests use for small ragged shapes. Returns a dict with the tensors and
-    the call parameters (ignore_index, reduction, dtype).
+    the tests use for small ragged shapes; ``dtype`` overrides the element type
+    (the same float64 draws, rounded to that type). Returns a dict with the
+    tensors and the call parameters (ignore_index, reduction, dtype).
     """
     w = WORKLOADS[name]
+    if dtype is not None:
+        w = dataclasses.replace(w, dtype=dtype)
     N = w.N if N is None else N
     H = w.H if H is None else H
     V = w.V if V is None else V
@@ -167,7 +171,7 @@ def random_case(N: int, H: int, V: int, dtype: str = "bf16", seed: int = 0,
                 ignore_index: int = IGNORE_INDEX):
     """A small ad-hoc case: hidden ~ x_scale*N(0,1), W ~ w_std*N(0,1), uniform labels."""
     rx, rw, ry, rm = _streams(seed)
-    tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+    tdtype = TORCH_DTYPES[dtype]
     hidden = torch.from_numpy(rx.standard_normal((N, H)) * x_scale).to(tdtype)
     weight = torch.from_numpy(rw.standard_normal((V, H)) * w_std).to(tdtype)
     labels = ry.integers(0, V, size=N, dtype=np.int64)
