@@ -5,7 +5,8 @@
 One step = one lce_forward_backward call (loss, dH, dW) over the whole synthetic batch, inputs
 already resident in HBM. Prints ONE JSON line with tokens/s, the fraction of the bf16 dense MFMA
 peak (credited work 6*N*H*V), the live roofline of the dominant kernel (HIP events recorded by the
-library on its launch stream), the forward-only rate (loss without gradients, 2*N*H*V), peak
+library on its launch stream), the forward-only rate (loss without gradients, 2*N*H*V), the step
+with the final RMSNorm fused in front (lce_rmsnorm_forward_backward), peak
 device memory against a materialised-logits PyTorch baseline, and the float64 CPU oracle timed on
 a bounded sample of the same workload.
 """
@@ -136,6 +137,7 @@ def main():
     ap.add_argument("--cpu-sample-tokens", type=int, default=3072)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
+    ap.add_argument("--no-rmsnorm", action="store_true", help="skip timing the variant with the final RMSNorm")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run plain copies of this many MiB (yardstick for HBM byte counters)")
     args = ap.parse_args()
@@ -223,6 +225,27 @@ def main():
                     "mfma_peak_frac": round(2.0 * N * H * V / (fms * 1e-3) / 1e12 / peak, 4)}
     log(f"forward only: {fms:.3f} ms/call")
 
+    # The same step with the final RMSNorm in front (pre-norm rows and a gain drawn by the generator).
+    rmsnorm = None
+    if not args.no_rmsnorm:
+        r = workloads.make_rmsnorm_inputs(args.workload, seed=0, dtype=args.dtype, base=d)
+        h, gam = r["hidden"].to(dev), r["gamma"].to(dev)
+        rws = torch.empty(lce.rmsnorm_workspace_size(N, H, V, dtype, True, args.chunk), dtype=torch.uint8, device=dev)
+        for _ in range(2):
+            lce.rmsnorm_forward_backward(h, gam, W, y, r["eps"], d["ignore_index"], d["reduction"], args.chunk, rws)
+        torch.cuda.synchronize()
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        r0.record(stream)
+        for _ in range(args.steps):
+            lce.rmsnorm_forward_backward(h, gam, W, y, r["eps"], d["ignore_index"], d["reduction"], args.chunk, rws)
+        r1.record(stream)
+        torch.cuda.synchronize()
+        rms = r0.elapsed_time(r1) / args.steps
+        rmsnorm = {"ms_per_step": round(rms, 4), "tokens_per_s": round(N / (rms * 1e-3), 1),
+                   "extra_ms_vs_lce": round(rms - ms, 4)}
+        del h, gam, rws
+        log(f"with the final RMSNorm fused: {rms:.3f} ms/step")
+
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
 
@@ -244,7 +267,7 @@ def main():
         "config": {"workload": args.workload if args.dtype is None else f"{args.workload}_{args.dtype}",
                    "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
-        "roofline": roofline, "forward_only": forward_only, "memory": memory,
+        "roofline": roofline, "forward_only": forward_only, "rmsnorm_fused": rmsnorm, "memory": memory,
     }
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host cores ...")

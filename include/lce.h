@@ -107,12 +107,51 @@ lce_status_t lce_forward_backward(const void* hidden, const void* weight, const 
                                   void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The final RMSNorm fused into the step. Section 3.3 ("Optimized Triton Kernels") names RMSNorm
+ * among the fused kernels; the normalisation right before the output layer is applied here,
+ * in the same call and on the same stream:
+ *
+ *     r_i = 1 / sqrt(mean_j h_ij^2 + eps),   x_ij = gamma_j h_ij r_i
+ *
+ * then the LCE step above on x. The backward adds the normalisation's Jacobian:
+ *     grad_hidden_ij = r_i gamma_j dX_ij - r_i^3 h_ij (1/H) sum_k h_ik gamma_k dX_ik
+ *     grad_gamma_j   = sum_i dX_ij h_ij r_i            (dX = d loss / d x)
+ *
+ *   hidden      : device [N,H] of dtype, the rows BEFORE normalisation.
+ *   gamma       : device [H] of dtype (the learned gain).
+ *   eps         : >= 0 and finite, else LCE_ERR_INVALID_ARGUMENT.
+ *   normed      : forward only, optional device [N,H] of dtype that receives x (NULL: x stays in
+ *                 the workspace).
+ *   grad_hidden : device [N,H] of dtype, gradient with respect to the pre-norm rows;
+ *   grad_gamma  : device [H] of dtype;  grad_weight: device [V,H] of dtype.
+ * Every other argument, convention and error is that of lce_forward / lce_forward_backward. The
+ * workspace is lce_rmsnorm_workspace_size(...) bytes: the step's own plus x [N,H] (dtype), r [N]
+ * and, with backward, dX [N,H] in fp32 (dX never passes through the input dtype), the dH GEMM's
+ * fp32 partials for one chunk, s [N] and [ceil(N/64), H] fp32 partials of grad_gamma (summed in a
+ * fixed order): O(N H), no N x V term.
+ */
+size_t lce_rmsnorm_workspace_size(int64_t N, int64_t H, int64_t V, int dtype, int with_backward,
+                                  int64_t chunk_tokens);
+lce_status_t lce_rmsnorm_forward(const void* hidden, const void* gamma, const void* weight,
+                                 const int64_t* labels, int64_t N, int64_t H, int64_t V, int dtype,
+                                 float eps, int64_t ignore_index, int reduction,
+                                 float* loss, float* lse, void* normed,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+lce_status_t lce_rmsnorm_forward_backward(const void* hidden, const void* gamma, const void* weight,
+                                          const int64_t* labels, int64_t N, int64_t H, int64_t V,
+                                          int dtype, float eps, int64_t ignore_index, int reduction,
+                                          float* loss, void* grad_hidden, void* grad_gamma,
+                                          void* grad_weight, int64_t chunk_tokens,
+                                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Per-kernel timing, for measurement tools (not for concurrent use). While enabled, every launch of
- * lce_forward / lce_forward_backward is bracketed by two hipEvents recorded on the call's stream.
+ * lce_forward / lce_forward_backward (and of their RMSNorm variants) is bracketed by two hipEvents
+ * recorded on the call's stream.
  * lce_timing_read waits for the recorded events and returns, per kernel kind, the total elapsed
  * milliseconds and the number of launches since the last enable; the events are then released.
  * Kinds: 0 logits GEMM + log-sum-exp, 1 dH GEMM (with its split reduction), 2 dW GEMM,
- * 3 dlogits, 4 transposes of W and X, 5 the remaining small kernels.
+ * 3 dlogits, 4 (unused), 5 the remaining small kernels (including the RMSNorm ones).
  * lce_timing_enable(1) resets the totals; (0) stops recording. Returns LCE_OK or LCE_ERR_HIP.
  */
 #define LCE_TIMING_KINDS 6

@@ -108,8 +108,10 @@ int64_t auto_chunk(int64_t N, int64_t H) {
 bool dtype_ok(int dtype) { return dtype == LCE_DTYPE_FP32 || dtype == LCE_DTYPE_BF16 || dtype == LCE_DTYPE_FP16; }
 
 // Fills `p`; returns LCE_OK or the status that the sizes deserve.
+// dx_f32: the caller wants d loss / d hidden in fp32 (through the split-K partials even with one
+// split), as the RMSNorm variant does.
 lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward, int64_t chunk_tokens,
-                       Plan& p, bool query_device) {
+                       Plan& p, bool query_device, bool dx_f32 = false) {
   if (N < 1 || H < 1 || V < 1 || !dtype_ok(dtype) || chunk_tokens < 0) return LCE_ERR_INVALID_ARGUMENT;
   p.N = N; p.H = H; p.V = V;
   p.esz = dtype == LCE_DTYPE_FP32 ? 4 : 2;
@@ -161,7 +163,7 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.o_psum = take((size_t)p.slices * p.ncp * 4);
   if (backward) {
     p.o_e = take((size_t)p.ncp * p.Vp * p.esz);
-    if (p.dh_splits > 1) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
+    if (p.dh_splits > 1 || dx_f32) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
   }
   p.total = off;
   return LCE_OK;
@@ -190,9 +192,10 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// dx32 (optional): receives d loss / d hidden in fp32 instead of dH (the plan must have dx_f32).
 template <typename T>
 lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_t ignore_index, int reduction,
-                 float* loss, float* lse_user, T* dH, T* dW, char* ws, hipStream_t s) {
+                 float* loss, float* lse_user, T* dH, T* dW, char* ws, hipStream_t s, float* dx32 = nullptr) {
   const int64_t N = p.N, H = p.H, V = p.V;
   int* nvalid = (int*)(ws + p.o_nvalid);
   float* tgt = (float*)(ws + p.o_tgt);
@@ -201,7 +204,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
   float* pmax = (float*)(ws + p.o_pmax);
   float* psum = (float*)(ws + p.o_psum);
   T* ez = p.backward ? (T*)(ws + p.o_e) : nullptr;
-  float* dhp = (p.backward && p.dh_splits > 1) ? (float*)(ws + p.o_dhp) : nullptr;
+  float* dhp = (p.backward && (p.dh_splits > 1 || dx32)) ? (float*)(ws + p.o_dhp) : nullptr;
   const int mean = reduction == LCE_REDUCTION_MEAN;
 
   {
@@ -259,7 +262,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     gh.K = (int)V;
     gh.splits = p.dh_splits; gh.k_per_split = (int)p.dh_kps;
     gh.group_m = 4;
-    if (p.dh_splits > 1) {
+    if (p.dh_splits > 1 || dx32) {
       gh.out = dhp; gh.ldo = H; gh.mode = 1;
     } else {
       gh.out = dH + t0 * H; gh.ldo = H; gh.mode = 0;
@@ -268,7 +271,12 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     {
     KernelTimer t(T_DH, s);
     if (launch_gemm<T, EPI_STORE, false, true>(gh, s) != hipSuccess) return LCE_ERR_HIP;
-    if (p.dh_splits > 1) {
+    if (dx32) {
+      const int64_t count = (int64_t)rows * H;
+      hipLaunchKernelGGL((split_reduce_kernel<float, T>), dim3((unsigned)cdiv(count / 4, 256)), dim3(256), 0, s, dhp,
+                         p.dh_splits, count, dx32 + t0 * H, (const int*)nvalid, mean);
+      if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+    } else if (p.dh_splits > 1) {
       const int64_t count = (int64_t)rows * H;
       hipLaunchKernelGGL((split_reduce_kernel<T>), dim3((unsigned)cdiv(count / 4, 256)), dim3(256), 0, s, dhp,
                          p.dh_splits, count, dH + t0 * H, (const int*)nvalid, mean);
@@ -296,6 +304,68 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     KernelTimer t(T_OTHER, s);
     hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, s, tl, N, nvalid, mean, loss);
   }
+  return hipGetLastError() == hipSuccess ? LCE_OK : LCE_ERR_HIP;
+}
+
+// The RMSNorm variant: the LCE plan, then x [N,H], r [N] and, for backward, dX [N,H] fp32, s [N]
+// and the dgamma partials [row blocks, H] (fp32) after it in the same workspace.
+struct RmsPlan {
+  Plan lce;
+  int64_t row_blocks = 0;
+  size_t o_x = 0, o_r = 0, o_dx = 0, o_s = 0, o_part = 0;
+  size_t total = 0;
+};
+
+lce_status_t make_rms_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward, int64_t chunk_tokens,
+                           RmsPlan& rp, bool query_device) {
+  lce_status_t st = make_plan(N, H, V, dtype, backward, chunk_tokens, rp.lce, query_device, backward);
+  if (st != LCE_OK) return st;
+  size_t off = rp.lce.total;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (size_t)round_up((int64_t)bytes, kAlign);
+    return o;
+  };
+  rp.o_x = take((size_t)N * H * rp.lce.esz);
+  rp.o_r = take((size_t)N * 4);
+  if (backward) {
+    rp.row_blocks = cdiv(N, kRmsRows);
+    rp.o_dx = take((size_t)N * H * 4);
+    rp.o_s = take((size_t)N * 4);
+    rp.o_part = take((size_t)rp.row_blocks * H * 4);
+  }
+  rp.total = off;
+  return LCE_OK;
+}
+
+bool eps_ok(float eps) { return eps >= 0.f && eps <= 3.0e38f; }  // rejects NaN and inf
+
+template <typename T>
+lce_status_t run_rms(const RmsPlan& rp, const T* h, const T* gamma, const T* W, const int64_t* y, float eps,
+                     int64_t ignore_index, int reduction, float* loss, float* lse, T* normed, T* dh, T* dgamma,
+                     T* dW, char* ws, hipStream_t s) {
+  const int64_t N = rp.lce.N, H = rp.lce.H;
+  T* x = normed ? normed : (T*)(ws + rp.o_x);
+  float* r = (float*)(ws + rp.o_r);
+  {
+    KernelTimer t(T_OTHER, s);
+    hipLaunchKernelGGL((rmsnorm_rows_kernel<T>), dim3((unsigned)cdiv(N, 4)), dim3(256), 0, s, h, gamma, N, H, eps, x,
+                       r);
+  }
+  if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+  // The LCE step on the normalised rows; its hidden gradient dX stays in fp32.
+  float* dx = rp.lce.backward ? (float*)(ws + rp.o_dx) : nullptr;
+  lce_status_t st = run<T>(rp.lce, x, W, y, ignore_index, reduction, loss, lse, nullptr, dW, ws, s, dx);
+  if (st != LCE_OK || !rp.lce.backward) return st;
+  KernelTimer t(T_OTHER, s);
+  float* srow = (float*)(ws + rp.o_s);
+  float* part = (float*)(ws + rp.o_part);
+  hipLaunchKernelGGL((rmsnorm_rowdot_kernel<T>), dim3((unsigned)cdiv(N, 4)), dim3(256), 0, s, h, gamma,
+                     (const float*)dx, N, H, srow);
+  hipLaunchKernelGGL((rmsnorm_backward_kernel<T>), dim3((unsigned)cdiv(H, 256), (unsigned)rp.row_blocks), dim3(256),
+                     0, s, h, gamma, (const float*)r, (const float*)srow, (const float*)dx, dh, N, H, part);
+  hipLaunchKernelGGL((rmsnorm_gamma_reduce_kernel<T>), dim3((unsigned)cdiv(H, 256)), dim3(256), 0, s,
+                     (const float*)part, (int)rp.row_blocks, H, dgamma);
   return hipGetLastError() == hipSuccess ? LCE_OK : LCE_ERR_HIP;
 }
 
@@ -358,6 +428,67 @@ lce_status_t lce_forward_backward(const void* hidden, const void* weight, const 
                               (char*)workspace, s);
   return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss,
                          nullptr, (float*)grad_hidden, (float*)grad_weight, (char*)workspace, s);
+}
+
+size_t lce_rmsnorm_workspace_size(int64_t N, int64_t H, int64_t V, int dtype, int with_backward,
+                                  int64_t chunk_tokens) {
+  lce::RmsPlan rp;
+  if (lce::make_rms_plan(N, H, V, dtype, with_backward != 0, chunk_tokens, rp, true) != LCE_OK) return 0;
+  return rp.total;
+}
+
+lce_status_t lce_rmsnorm_forward(const void* hidden, const void* gamma, const void* weight, const int64_t* labels,
+                                 int64_t N, int64_t H, int64_t V, int dtype, float eps, int64_t ignore_index,
+                                 int reduction, float* loss, float* lse, void* normed, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  if (!hidden || !gamma || !weight || !labels || !loss || !lce::eps_ok(eps)) return LCE_ERR_INVALID_ARGUMENT;
+  if (reduction != LCE_REDUCTION_NONE && reduction != LCE_REDUCTION_MEAN && reduction != LCE_REDUCTION_SUM)
+    return LCE_ERR_INVALID_ARGUMENT;
+  lce::RmsPlan rp;
+  lce_status_t st = lce::make_rms_plan(N, H, V, dtype, false, 0, rp, true);
+  if (st != LCE_OK) return st;
+  if (!workspace || workspace_bytes < rp.total) return LCE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if (dtype == LCE_DTYPE_BF16)
+    return lce::run_rms<lce::bf16>(rp, (const lce::bf16*)hidden, (const lce::bf16*)gamma, (const lce::bf16*)weight,
+                                   labels, eps, ignore_index, reduction, loss, lse, (lce::bf16*)normed, nullptr,
+                                   nullptr, nullptr, ws, s);
+  if (dtype == LCE_DTYPE_FP16)
+    return lce::run_rms<lce::f16>(rp, (const lce::f16*)hidden, (const lce::f16*)gamma, (const lce::f16*)weight,
+                                  labels, eps, ignore_index, reduction, loss, lse, (lce::f16*)normed, nullptr,
+                                  nullptr, nullptr, ws, s);
+  return lce::run_rms<float>(rp, (const float*)hidden, (const float*)gamma, (const float*)weight, labels, eps,
+                             ignore_index, reduction, loss, lse, (float*)normed, nullptr, nullptr, nullptr, ws, s);
+}
+
+lce_status_t lce_rmsnorm_forward_backward(const void* hidden, const void* gamma, const void* weight,
+                                          const int64_t* labels, int64_t N, int64_t H, int64_t V, int dtype,
+                                          float eps, int64_t ignore_index, int reduction, float* loss,
+                                          void* grad_hidden, void* grad_gamma, void* grad_weight,
+                                          int64_t chunk_tokens, void* workspace, size_t workspace_bytes,
+                                          void* stream) {
+  if (!hidden || !gamma || !weight || !labels || !loss || !grad_hidden || !grad_gamma || !grad_weight ||
+      !lce::eps_ok(eps))
+    return LCE_ERR_INVALID_ARGUMENT;
+  if (reduction != LCE_REDUCTION_MEAN && reduction != LCE_REDUCTION_SUM) return LCE_ERR_INVALID_ARGUMENT;
+  lce::RmsPlan rp;
+  lce_status_t st = lce::make_rms_plan(N, H, V, dtype, true, chunk_tokens, rp, true);
+  if (st != LCE_OK) return st;
+  if (!workspace || workspace_bytes < rp.total) return LCE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if (dtype == LCE_DTYPE_BF16)
+    return lce::run_rms<lce::bf16>(rp, (const lce::bf16*)hidden, (const lce::bf16*)gamma, (const lce::bf16*)weight,
+                                   labels, eps, ignore_index, reduction, loss, nullptr, nullptr,
+                                   (lce::bf16*)grad_hidden, (lce::bf16*)grad_gamma, (lce::bf16*)grad_weight, ws, s);
+  if (dtype == LCE_DTYPE_FP16)
+    return lce::run_rms<lce::f16>(rp, (const lce::f16*)hidden, (const lce::f16*)gamma, (const lce::f16*)weight,
+                                  labels, eps, ignore_index, reduction, loss, nullptr, nullptr,
+                                  (lce::f16*)grad_hidden, (lce::f16*)grad_gamma, (lce::f16*)grad_weight, ws, s);
+  return lce::run_rms<float>(rp, (const float*)hidden, (const float*)gamma, (const float*)weight, labels, eps,
+                             ignore_index, reduction, loss, nullptr, nullptr, (float*)grad_hidden,
+                             (float*)grad_gamma, (float*)grad_weight, ws, s);
 }
 
 lce_status_t lce_timing_enable(int enable) {

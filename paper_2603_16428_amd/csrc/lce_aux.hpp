@@ -141,9 +141,9 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
   }
 }
 
-// out[i][h] = sum_s part[s][i][h] (fixed order), times the dz storage scale's inverse (1 unless
-// dz is stored unscaled), converted to the output type.
-template <typename T>
+// out[i][h] = sum_s part[s][i][h] (fixed order), times the dz storage scale's inverse of the
+// operand type TS (1 unless dz is stored unscaled), converted to the output type T.
+template <typename T, typename TS = T>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int splits,
                                                            int64_t count, T* __restrict__ out,
                                                            const int* __restrict__ n_valid, int mean) {
@@ -154,8 +154,8 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
     const float4 v = *(const float4*)(part + (size_t)k * count + idx);
     s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
   }
-  if constexpr (Storage<T>::kDzUnscaled) {
-    const float sc = dz_epilogue_scale<T>(n_valid, mean);
+  if constexpr (Storage<TS>::kDzUnscaled) {
+    const float sc = dz_epilogue_scale<TS>(n_valid, mean);
     s.x *= sc; s.y *= sc; s.z *= sc; s.w *= sc;
   }
   out[idx] = from_f32<T>(s.x);
@@ -186,6 +186,103 @@ __global__ __launch_bounds__(1024) void loss_reduce_kernel(const float* __restri
     }
     *loss = (float)r;
   }
+}
+
+}  // namespace lce
+
+namespace lce {
+
+// ---- final RMSNorm around the step (x_i = gamma . h_i r_i, r_i = 1 / sqrt(mean_j h_ij^2 + eps)) ----
+
+// One wave per token: r_i, and the normalised row x_i in the input dtype (fp32 arithmetic).
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_rows_kernel(const T* __restrict__ h, const T* __restrict__ gamma,
+                                                           int64_t N, int64_t H, float eps, T* __restrict__ x,
+                                                           float* __restrict__ r_out) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  constexpr int kVec = 16 / sizeof(T);
+  const T* hr = h + i * H;
+  float ss = 0.f;
+  for (int64_t j = (int64_t)lane * kVec; j < H; j += 64 * kVec) {
+    T v[kVec];
+    *(uint4*)v = *(const uint4*)(hr + j);
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) ss = fmaf(to_f32(v[e]), to_f32(v[e]), ss);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  const float r = 1.f / sqrtf(ss / (float)H + eps);
+  T* xr = x + i * H;
+  for (int64_t j = (int64_t)lane * kVec; j < H; j += 64 * kVec) {
+    T v[kVec], gv[kVec], o[kVec];
+    *(uint4*)v = *(const uint4*)(hr + j);
+    *(uint4*)gv = *(const uint4*)(gamma + j);
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) o[e] = from_f32<T>(to_f32(gv[e]) * (to_f32(v[e]) * r));
+    *(uint4*)(xr + j) = *(const uint4*)o;
+  }
+  if (lane == 0) r_out[i] = r;
+}
+
+// One wave per token: s_i = sum_k h_ik gamma_k dX_ik (fp32, fixed order; dX in fp32).
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_rowdot_kernel(const T* __restrict__ h, const T* __restrict__ gamma,
+                                                             const float* __restrict__ dx, int64_t N, int64_t H,
+                                                             float* __restrict__ s_out) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  constexpr int kVec = 16 / sizeof(T);
+  float s = 0.f;
+  for (int64_t j = (int64_t)lane * kVec; j < H; j += 64 * kVec) {
+    T hv[kVec], gv[kVec];
+    *(uint4*)hv = *(const uint4*)(h + i * H + j);
+    *(uint4*)gv = *(const uint4*)(gamma + j);
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) s = fmaf(to_f32(hv[e]) * to_f32(gv[e]), dx[i * H + j + e], s);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) s_out[i] = s;
+}
+
+// The Jacobian, from the fp32 dX rows into the gradient rows, kRmsRows tokens x 256 features per block:
+//   dh_ij = r_i gamma_j dX_ij - r_i^3 h_ij s_i / H,   and the block's share of
+//   dgamma_j = sum_i dX_ij h_ij r_i, written to part[blockIdx.y][j] (summed in a fixed order later).
+constexpr int kRmsRows = 64;
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_backward_kernel(const T* __restrict__ h, const T* __restrict__ gamma,
+                                                               const float* __restrict__ r, const float* __restrict__ s,
+                                                               const float* __restrict__ dx, T* __restrict__ g,
+                                                               int64_t N, int64_t H, float* __restrict__ part) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t i0 = (int64_t)blockIdx.y * kRmsRows;
+  if (j >= H) return;
+  const float gj = to_f32(gamma[j]);
+  const float invH = 1.f / (float)H;
+  float dg = 0.f;
+  const int64_t i1 = i0 + kRmsRows < N ? i0 + kRmsRows : N;
+  for (int64_t i = i0; i < i1; ++i) {
+    const float ri = r[i];
+    const float hij = to_f32(h[i * H + j]);
+    const float dxij = dx[i * H + j];
+    dg = fmaf(dxij * hij, ri, dg);
+    g[i * H + j] = from_f32<T>(ri * gj * dxij - ri * ri * ri * hij * s[i] * invH);
+  }
+  part[(size_t)blockIdx.y * H + j] = dg;
+}
+
+// dgamma_j = sum over row blocks of part[b][j], in block order.
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_gamma_reduce_kernel(const float* __restrict__ part, int blocks,
+                                                                   int64_t H, T* __restrict__ dgamma) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= H) return;
+  float acc = 0.f;
+  for (int b = 0; b < blocks; ++b) acc += part[(size_t)b * H + j];
+  dgamma[j] = from_f32<T>(acc);
 }
 
 }  // namespace lce

@@ -21,6 +21,7 @@ STATUS = {0: "LCE_OK", 1: "LCE_ERR_INVALID_ARGUMENT", 2: "LCE_ERR_UNSUPPORTED",
 DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
 EXPORTED = ("lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
+            "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward", "lce_rmsnorm_forward_backward",
             "lce_timing_enable", "lce_timing_read", "lce_status_string")
 TIMING_KINDS = ("logits_lse_gemm", "dh_gemm", "dw_gemm", "dlogits", "transpose", "other")
 
@@ -51,6 +52,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.lce_forward_backward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp,
                                          i64, vp, sz, vp]
     lib.lce_forward_backward.restype = ctypes.c_int
+    f32 = ctypes.c_float
+    lib.lce_rmsnorm_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, ctypes.c_int, i64]
+    lib.lce_rmsnorm_workspace_size.restype = sz
+    lib.lce_rmsnorm_forward.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, f32, i64, ctypes.c_int,
+                                        vp, vp, vp, vp, sz, vp]
+    lib.lce_rmsnorm_forward.restype = ctypes.c_int
+    lib.lce_rmsnorm_forward_backward.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, f32, i64,
+                                                 ctypes.c_int, vp, vp, vp, vp, i64, vp, sz, vp]
+    lib.lce_rmsnorm_forward_backward.restype = ctypes.c_int
     lib.lce_timing_enable.argtypes = [ctypes.c_int]
     lib.lce_timing_enable.restype = ctypes.c_int
     lib.lce_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
@@ -187,3 +197,96 @@ class LinearCrossEntropy(torch.autograd.Function):
 
 def linear_cross_entropy(hidden, weight, labels, ignore_index: int = -100, reduction: str = "mean"):
     return LinearCrossEntropy.apply(hidden, weight, labels, ignore_index, reduction)
+
+
+# ---- the final RMSNorm fused into the step --------------------------------------------------------
+
+def _check_gamma(gamma, hidden):
+    if gamma.dtype != hidden.dtype or gamma.dim() != 1 or gamma.shape[0] != hidden.shape[1]:
+        raise ValueError("gamma must be [H] of the hidden dtype")
+    if not gamma.is_contiguous() or gamma.device != hidden.device:
+        raise ValueError("gamma must be contiguous and on the hidden's device")
+
+
+def rmsnorm_workspace_size(N: int, H: int, V: int, dtype=torch.bfloat16, with_backward: bool = True,
+                           chunk_tokens: int = 0) -> int:
+    return int(load_library().lce_rmsnorm_workspace_size(N, H, V, DTYPES[dtype], int(with_backward), chunk_tokens))
+
+
+def rmsnorm_forward(hidden, gamma, weight, labels, eps: float = 1e-5, ignore_index: int = -100,
+                    reduction: str = "mean", return_lse: bool = False, return_normed: bool = False,
+                    workspace: torch.Tensor | None = None):
+    """Loss of the step on x = RMSNorm(hidden) * gamma; optionally each token's lse and x itself."""
+    lib = load_library()
+    N, H, V = _check_inputs(hidden, weight, labels)
+    _check_gamma(gamma, hidden)
+    dt = DTYPES[hidden.dtype]
+    red = REDUCTIONS[reduction]
+    need = lib.lce_rmsnorm_workspace_size(N, H, V, dt, 0, 0)
+    if need == 0:
+        raise LCEError(2, "lce_rmsnorm_workspace_size")
+    ws = workspace if workspace is not None else _workspace(need, hidden.device)
+    loss = torch.empty(N if red == 0 else 1, dtype=torch.float32, device=hidden.device)
+    lse = torch.empty(N, dtype=torch.float32, device=hidden.device) if return_lse else None
+    normed = torch.empty_like(hidden) if return_normed else None
+    stream = ctypes.c_void_p(torch.cuda.current_stream(hidden.device).cuda_stream)
+    st = lib.lce_rmsnorm_forward(_ptr(hidden), _ptr(gamma), _ptr(weight), _ptr(labels), N, H, V, dt, float(eps),
+                                 ignore_index, red, _ptr(loss), _ptr(lse), _ptr(normed), _ptr(ws), ws.numel(), stream)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_rmsnorm_forward")
+    out = (loss if red == 0 else loss[0],)
+    if return_lse:
+        out += (lse,)
+    if return_normed:
+        out += (normed,)
+    return out if len(out) > 1 else out[0]
+
+
+def rmsnorm_forward_backward(hidden, gamma, weight, labels, eps: float = 1e-5, ignore_index: int = -100,
+                             reduction: str = "mean", chunk_tokens: int = 0,
+                             workspace: torch.Tensor | None = None):
+    """(loss, grad_hidden, grad_gamma, grad_weight); grad_hidden is with respect to the pre-norm rows."""
+    lib = load_library()
+    N, H, V = _check_inputs(hidden, weight, labels)
+    _check_gamma(gamma, hidden)
+    dt = DTYPES[hidden.dtype]
+    red = REDUCTIONS[reduction]
+    need = lib.lce_rmsnorm_workspace_size(N, H, V, dt, 1, chunk_tokens)
+    if need == 0:
+        raise LCEError(2, "lce_rmsnorm_workspace_size")
+    ws = workspace if workspace is not None else _workspace(need, hidden.device)
+    loss = torch.empty(1, dtype=torch.float32, device=hidden.device)
+    dh = torch.empty_like(hidden)
+    dg = torch.empty_like(gamma)
+    dW = torch.empty_like(weight)
+    stream = ctypes.c_void_p(torch.cuda.current_stream(hidden.device).cuda_stream)
+    st = lib.lce_rmsnorm_forward_backward(_ptr(hidden), _ptr(gamma), _ptr(weight), _ptr(labels), N, H, V, dt,
+                                          float(eps), ignore_index, red, _ptr(loss), _ptr(dh), _ptr(dg), _ptr(dW),
+                                          chunk_tokens, _ptr(ws), ws.numel(), stream)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_rmsnorm_forward_backward")
+    return loss[0], dh, dg, dW
+
+
+class RMSNormLinearCrossEntropy(torch.autograd.Function):
+    """loss = cross_entropy(rms_norm(hidden, gamma, eps) @ weight.T, labels), fused, without logits."""
+
+    @staticmethod
+    def forward(ctx, hidden, gamma, weight, labels, eps=1e-5, ignore_index=-100, reduction="mean"):
+        if hidden.requires_grad or gamma.requires_grad or weight.requires_grad:
+            loss, dh, dg, dW = rmsnorm_forward_backward(hidden, gamma, weight, labels, eps, ignore_index, reduction)
+            ctx.save_for_backward(dh, dg, dW)
+        else:
+            loss = rmsnorm_forward(hidden, gamma, weight, labels, eps, ignore_index, reduction)
+        return loss
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        dh, dg, dW = ctx.saved_tensors
+        g = grad_out.to(torch.float32)
+        return (dh * g).to(dh.dtype), (dg * g).to(dg.dtype), (dW * g).to(dW.dtype), None, None, None, None
+
+
+def rmsnorm_linear_cross_entropy(hidden, gamma, weight, labels, eps: float = 1e-5, ignore_index: int = -100,
+                                 reduction: str = "mean"):
+    return RMSNormLinearCrossEntropy.apply(hidden, gamma, weight, labels, eps, ignore_index, reduction)

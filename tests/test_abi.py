@@ -31,7 +31,8 @@ def _declared_functions():
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward",
-                            "lce_forward_backward", "lce_timing_enable", "lce_timing_read",
+                            "lce_forward_backward", "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward",
+                            "lce_rmsnorm_forward_backward", "lce_timing_enable", "lce_timing_read",
                             "lce_status_string"])
     for n in names:
         assert hasattr(lib, n), n
@@ -108,3 +109,55 @@ def test_forward_validation(lib, kw, status):
 ])
 def test_forward_backward_validation(lib, kw, status):
     assert _fb(lib, **kw) == status
+
+
+# ---- the RMSNorm variant -------------------------------------------------------------------------
+
+def test_rmsnorm_workspace_size(lib):
+    ws = lib.lce_rmsnorm_workspace_size
+    assert ws(0, 8, 8, BF16, 1, 0) == 0
+    assert ws(8, 12, 8, BF16, 1, 0) == 0           # same shape rules as the plain step
+    base = lib.lce_workspace_size(8192, 4096, 128256, BF16, 1, 0)
+    extra = ws(8192, 4096, 128256, BF16, 1, 0) - base
+    # x [N,H] bf16, dX [N,H] fp32, one chunk's fp32 dH partials (4096 x 4096 here), r and s [N],
+    # ceil(N/64) x H fp32 partials (+ alignment): O(N H), no N x V.
+    top = 8192 * 4096 * (2 + 4) + 4096 * 4096 * 4 + 2 * 8192 * 4 + 128 * 4096 * 4 + 8 * 256
+    assert 8192 * 4096 * 6 <= extra <= top
+    fwd = ws(8192, 4096, 128256, BF16, 0, 0) - lib.lce_workspace_size(8192, 4096, 128256, BF16, 0, 0)
+    assert 8192 * 4096 * 2 <= fwd < extra
+
+
+def _rfwd(lib, **kw):
+    a = dict(hidden=FAKE, gamma=FAKE, weight=FAKE, labels=FAKE, N=16, H=64, V=100, dtype=BF16, eps=1e-5,
+             ignore=-100, red=MEAN, loss=FAKE, lse=None, normed=None, ws=FAKE, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return lib.lce_rmsnorm_forward(a["hidden"], a["gamma"], a["weight"], a["labels"], a["N"], a["H"], a["V"],
+                                   a["dtype"], a["eps"], a["ignore"], a["red"], a["loss"], a["lse"], a["normed"],
+                                   a["ws"], a["wsb"], a["stream"])
+
+
+def _rfb(lib, **kw):
+    a = dict(hidden=FAKE, gamma=FAKE, weight=FAKE, labels=FAKE, N=16, H=64, V=100, dtype=BF16, eps=1e-5,
+             ignore=-100, red=MEAN, loss=FAKE, dh=FAKE, dg=FAKE, dw=FAKE, chunk=0, ws=FAKE, wsb=1 << 30,
+             stream=None)
+    a.update(kw)
+    return lib.lce_rmsnorm_forward_backward(a["hidden"], a["gamma"], a["weight"], a["labels"], a["N"], a["H"],
+                                            a["V"], a["dtype"], a["eps"], a["ignore"], a["red"], a["loss"],
+                                            a["dh"], a["dg"], a["dw"], a["chunk"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(gamma=None), INVALID), (dict(hidden=None), INVALID), (dict(eps=-1.0), INVALID),
+    (dict(eps=float("nan")), INVALID), (dict(eps=float("inf")), INVALID), (dict(red=3), INVALID),
+    (dict(H=60), UNSUPPORTED), (dict(wsb=16), WS_SMALL),
+])
+def test_rmsnorm_forward_validation(lib, kw, status):
+    assert _rfwd(lib, **kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dg=None), INVALID), (dict(dh=None), INVALID), (dict(dw=None), INVALID), (dict(red=NONE), INVALID),
+    (dict(eps=-0.5), INVALID), (dict(H=20), UNSUPPORTED), (dict(wsb=0), WS_SMALL),
+])
+def test_rmsnorm_forward_backward_validation(lib, kw, status):
+    assert _rfb(lib, **kw) == status

@@ -103,3 +103,12 @@ def test_zero_gamma():
     assert abs(out["loss"] - np.log(11)) <= 1e-13
     assert np.all(out["dh"] == 0.0)
     assert np.any(out["dgamma"] != 0.0)
+
+
+def test_sampled_rows_match_full_result():
+    h, gamma, W, y = _case(11, 9, 15, seed=6)
+    full = orn.forward_backward(h, gamma, W, y, eps=1e-4)
+    g, _ = oracle.token_weights(y, -100, "mean", 15)
+    rows = [0, 3, 7, 10]
+    np.testing.assert_allclose(orn.grad_hidden_rows(h, gamma, W, y, rows, g, eps=1e-4), full["dh"][rows],
+                               rtol=1e-11, atol=1e-15)

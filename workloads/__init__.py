@@ -156,10 +156,35 @@ def make_inputs(name: str, seed: int = 0, N: int | None = None, H: int | None = 
     }
 
 
+def make_rmsnorm_inputs(name: str, seed: int = 0, N: int | None = None, H: int | None = None,
+                        V: int | None = None, dtype: str | None = None, base: dict | None = None):
+    """Inputs of the step with the final RMSNorm in front: ``make_inputs`` plus pre-norm rows and a gain.
+
+    The pre-norm rows are the workload's hidden draws (before rounding) times a per-token scale
+    drawn log-uniformly in [0.25, 16] (the residual stream's magnitude varies by token), rounded to
+    the dtype; the gain is 1 + 0.1 N(0, 1) per feature. Both come from a fifth stream of the seed
+    (child 4 of the same SeedSequence), so weight, labels and the mask are those of ``make_inputs``;
+    ``base``, the result of that very ``make_inputs`` call, saves drawing them again.
+    """
+    d = dict(base) if base is not None else make_inputs(name, seed, N, H, V, dtype)
+    w = WORKLOADS[name]
+    rx = _streams(seed)[0]
+    g = _hidden(rx, w, d["N"], d["H"])                   # the same float64 draws as d["hidden"]
+    extra = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed).spawn(5)[4]))
+    scale = np.exp(extra.uniform(np.log(0.25), np.log(16.0), size=(d["N"], 1)))
+    gamma = 1.0 + 0.1 * extra.standard_normal(d["H"])
+    tdtype = TORCH_DTYPES[d["dtype"]]
+    d["hidden"] = torch.from_numpy(g * scale).to(tdtype)
+    d["gamma"] = torch.from_numpy(gamma).to(tdtype)
+    d["eps"] = 1e-5
+    d["name"] = f"{name}_rmsnorm"
+    return d
+
+
 def fingerprint(inputs) -> str:
     """SHA-256 over the raw bytes of hidden, weight and labels."""
     h = hashlib.sha256()
-    for key in ("hidden", "weight", "labels"):
+    for key in ("hidden", "weight", "labels") + (("gamma",) if "gamma" in inputs else ()):
         t = inputs[key].contiguous()
         h.update(t.view(torch.uint8).numpy().tobytes() if t.dtype != torch.int64
                  else t.numpy().tobytes())
