@@ -145,6 +145,29 @@ lce_status_t lce_rmsnorm_forward_backward(const void* hidden, const void* gamma,
                                           void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Host optimizer step for the output layer's FP32 master weights (Section 3.2, "Layer-Adam
+ * Optimizer"; schedule in Section 3.1, "Asynchronous Parameter Updating"). AdamW with bias
+ * correction, t = step (from 1):
+ *     m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2
+ *     p = p - lr ( (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps) + weight_decay p )
+ * in fp32, updating param, exp_avg and exp_avg_sq in place (all HOST memory, n elements). grad has
+ * the element type `dtype` (BF16, FP16 or FP32), typically the pinned buffer a gradient was copied
+ * into from the GPU. If param16 is not NULL (16-bit dtypes only) the updated parameters are also
+ * written there, rounded to `dtype` (the shared conversion buffer of Section 3.2, "Optimized CPU
+ * Memory Layout with Shared Buffers", ready for the next h2d copy). n_threads: CPU threads to split
+ * the range over (0 = all hardware threads). Returns after the update (no GPU work; no allocation
+ * beyond the threads). Errors: LCE_ERR_INVALID_ARGUMENT for a null pointer, n < 0, step < 1,
+ * an unknown dtype, param16 with FP32, or lr < 0, beta outside [0, 1), eps <= 0, weight_decay < 0
+ * or any non-finite setting.
+ */
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+} lce_adam_config_t;
+lce_status_t lce_host_adam_step(float* param, const void* grad, int dtype, float* exp_avg,
+                                float* exp_avg_sq, int64_t n, const lce_adam_config_t* cfg,
+                                int64_t step, void* param16, int n_threads);
+
+/*
  * Per-kernel timing, for measurement tools (not for concurrent use). While enabled, every launch of
  * lce_forward / lce_forward_backward (and of their RMSNorm variants) is bracketed by two hipEvents
  * recorded on the call's stream.

@@ -1,10 +1,10 @@
 """Fused linear + cross-entropy (output projection and loss) for MI355X, in HIP."""
-from .lce import (LCEError, LinearCrossEntropy, RMSNormLinearCrossEntropy, auto_chunk_tokens, forward,
-                  forward_backward, linear_cross_entropy, load_library, rmsnorm_forward,
+from .lce import (AdamConfig, LCEError, LinearCrossEntropy, RMSNormLinearCrossEntropy, auto_chunk_tokens, forward,
+                  forward_backward, host_adam_step, linear_cross_entropy, load_library, rmsnorm_forward,
                   rmsnorm_forward_backward, rmsnorm_linear_cross_entropy, rmsnorm_workspace_size, timing_enable,
                   timing_read, workspace_size)
 
-__all__ = ["LCEError", "LinearCrossEntropy", "RMSNormLinearCrossEntropy", "auto_chunk_tokens", "forward",
-           "forward_backward", "linear_cross_entropy", "load_library", "rmsnorm_forward",
+__all__ = ["AdamConfig", "LCEError", "LinearCrossEntropy", "RMSNormLinearCrossEntropy", "auto_chunk_tokens", "forward",
+           "forward_backward", "host_adam_step", "linear_cross_entropy", "load_library", "rmsnorm_forward",
            "rmsnorm_forward_backward", "rmsnorm_linear_cross_entropy", "rmsnorm_workspace_size", "timing_enable",
            "timing_read", "workspace_size"]

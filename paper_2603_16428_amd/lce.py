@@ -22,10 +22,17 @@ DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
 EXPORTED = ("lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
             "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward", "lce_rmsnorm_forward_backward",
+            "lce_host_adam_step",
             "lce_timing_enable", "lce_timing_read", "lce_status_string")
 TIMING_KINDS = ("logits_lse_gemm", "dh_gemm", "dw_gemm", "dlogits", "transpose", "other")
 
 _lib = None
+
+
+class AdamConfig(ctypes.Structure):
+    """lce_adam_config_t."""
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
 
 
 class LCEError(RuntimeError):
@@ -61,6 +68,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.lce_rmsnorm_forward_backward.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, f32, i64,
                                                  ctypes.c_int, vp, vp, vp, vp, i64, vp, sz, vp]
     lib.lce_rmsnorm_forward_backward.restype = ctypes.c_int
+    lib.lce_host_adam_step.argtypes = [vp, vp, ctypes.c_int, vp, vp, i64, ctypes.POINTER(AdamConfig), i64, vp,
+                                       ctypes.c_int]
+    lib.lce_host_adam_step.restype = ctypes.c_int
     lib.lce_timing_enable.argtypes = [ctypes.c_int]
     lib.lce_timing_enable.restype = ctypes.c_int
     lib.lce_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
@@ -290,3 +300,27 @@ class RMSNormLinearCrossEntropy(torch.autograd.Function):
 def rmsnorm_linear_cross_entropy(hidden, gamma, weight, labels, eps: float = 1e-5, ignore_index: int = -100,
                                  reduction: str = "mean"):
     return RMSNormLinearCrossEntropy.apply(hidden, gamma, weight, labels, eps, ignore_index, reduction)
+
+
+# ---- host optimizer step --------------------------------------------------------------------------
+
+def host_adam_step(param, grad, exp_avg, exp_avg_sq, step: int, lr: float, betas=(0.9, 0.999), eps: float = 1e-8,
+                   weight_decay: float = 0.0, param16=None, threads: int = 0) -> None:
+    """AdamW on host fp32 tensors in place (grad: host bf16/fp16/fp32); optionally writes param16."""
+    lib = load_library()
+    for t in (param, exp_avg, exp_avg_sq):
+        if t.device.type != "cpu" or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("param and states must be contiguous host float32 tensors")
+    n = param.numel()
+    if grad.device.type != "cpu" or grad.numel() != n or not grad.is_contiguous() or grad.dtype not in DTYPES:
+        raise ValueError("grad must be a contiguous host tensor of the same size")
+    if exp_avg.numel() != n or exp_avg_sq.numel() != n:
+        raise ValueError("state sizes differ from the parameter's")
+    if param16 is not None and (param16.dtype != grad.dtype or param16.numel() != n or param16.device.type != "cpu"
+                                or not param16.is_contiguous()):
+        raise ValueError("param16 must be a contiguous host tensor of the gradient's dtype")
+    cfg = AdamConfig(lr, betas[0], betas[1], eps, weight_decay)
+    st = lib.lce_host_adam_step(_ptr(param), _ptr(grad), DTYPES[grad.dtype], _ptr(exp_avg), _ptr(exp_avg_sq), n,
+                                ctypes.byref(cfg), step, _ptr(param16), threads)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_host_adam_step")

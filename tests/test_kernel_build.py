@@ -26,7 +26,7 @@ GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li{e}ELb{a}ELb{b}EEEvNS_8GemmArgsE"
 @pytest.fixture(scope="module")
 def asm():
     with tempfile.TemporaryDirectory() as d:
-        cmd = [B.HIPCC] + [f for f in B.FLAGS if f != "-shared"] + ["-c", "--save-temps"] + B.SOURCES + \
+        cmd = [B.HIPCC] + [f for f in B.FLAGS if f != "-shared"] + ["-c", "--save-temps"] + B.KERNEL_SOURCES + \
               ["-o", os.path.join(d, "lce.o")]
         r = subprocess.run(cmd, cwd=d, capture_output=True, text=True)
         assert r.returncode == 0, r.stderr[-2000:]
