@@ -32,8 +32,8 @@ def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward",
                             "lce_forward_backward", "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward",
-                            "lce_rmsnorm_forward_backward", "lce_timing_enable", "lce_timing_read",
-                            "lce_status_string"])
+                            "lce_rmsnorm_forward_backward", "lce_host_adam_step", "lce_timing_enable",
+                            "lce_timing_read", "lce_status_string"])
     for n in names:
         assert hasattr(lib, n), n
 
