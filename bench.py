@@ -6,7 +6,8 @@ One step = one lce_forward_backward call (loss, dH, dW) over the whole synthetic
 already resident in HBM. Prints ONE JSON line with tokens/s, the fraction of the bf16 dense MFMA
 peak (credited work 6*N*H*V), the live roofline of the dominant kernel (HIP events recorded by the
 library on its launch stream), the forward-only rate (loss without gradients, 2*N*H*V), the step
-with the final RMSNorm fused in front (lce_rmsnorm_forward_backward), peak
+with the final RMSNorm fused in front (lce_rmsnorm_forward_backward), a training step of the output
+layer with host-resident weights and its hiding factor (lce_head_train_step), peak
 device memory against a materialised-logits PyTorch baseline, and the float64 CPU oracle timed on
 a bounded sample of the same workload.
 """
@@ -19,6 +20,8 @@ import os
 import re
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -138,6 +141,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
     ap.add_argument("--no-rmsnorm", action="store_true", help="skip timing the variant with the final RMSNorm")
+    ap.add_argument("--no-head-train", action="store_true",
+                    help="skip the output-layer training step with host-resident weights")
+    ap.add_argument("--vocab-blocks", type=int, default=8, help="pipeline blocks of the head training step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run plain copies of this many MiB (yardstick for HBM byte counters)")
     args = ap.parse_args()
@@ -170,6 +176,7 @@ def main():
     lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
     torch.cuda.synchronize()
     lce_peak = torch.cuda.max_memory_allocated() - base
+    ws_keep = ws
 
     for _ in range(args.warmup):
         lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
@@ -246,12 +253,38 @@ def main():
         del h, gam, rws
         log(f"with the final RMSNorm fused: {rms:.3f} ms/step")
 
+    # A training step of the output layer with its weights in host memory (FP32 master, AdamW on
+    # the CPU, 16-bit pinned gradient and parameter buffers), pipelined over vocabulary blocks, and
+    # the same work run phase after phase. Hiding factor eta = T_bwd / (T_d2h + T_update).
+    head = None
+    if not args.no_head_train and dtype != torch.float32:
+        threads = min(16, len(os.sched_getaffinity(0)))
+        st = lce.HeadState(W.clone())
+        kw = dict(lr=1e-4, betas=(0.9, 0.95), weight_decay=0.01, ignore_index=d["ignore_index"],
+                  reduction=d["reduction"], chunk_tokens=args.chunk, vocab_blocks=args.vocab_blocks,
+                  threads=threads, workspace=ws_keep)
+        rec = {}
+        for name, overlap in (("pipelined", True), ("sequential", False)):
+            lce.head_train_step(st, X, y, overlap=overlap, **kw)
+            runs = [lce.head_train_step(st, X, y, overlap=overlap, **kw)[2] for _ in range(3)]
+            rec[name] = {k: round(float(np.median([r[k] for r in runs])), 3) for k in runs[0]}
+        p_ = rec["pipelined"]
+        bwd = p_["gpu_ms"] - fms
+        head = {"vocab_blocks": args.vocab_blocks, "threads": threads, "pipelined_ms": p_["step_ms"],
+                "sequential_ms": rec["sequential"]["step_ms"], "gpu_ms": p_["gpu_ms"], "bwd_ms": round(bwd, 3),
+                "d2h_ms": p_["d2h_ms"], "update_ms": p_["update_ms"], "h2d_ms": p_["h2d_ms"],
+                "tail_ms": p_["tail_ms"], "eta": round(bwd / (p_["d2h_ms"] + p_["update_ms"]), 4),
+                "phases_sequential": rec["sequential"]}
+        del st
+        log(f"head train step: pipelined {p_['step_ms']:.1f} ms, sequential {rec['sequential']['step_ms']:.1f} ms, "
+            f"d2h {p_['d2h_ms']:.1f} ms, update {p_['update_ms']:.1f} ms, eta {head['eta']:.3f}")
+
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
 
     memory = {"lce_peak_bytes": int(lce_peak)}
     if not args.no_memory:
-        del ws
+        del ws, ws_keep
         torch.cuda.empty_cache()
         mpeak, mtime = materialised_baseline(X, W, y, d["ignore_index"], d["reduction"])
         memory.update({"materialised_peak_bytes": int(mpeak), "reduction_vs_materialised": round(1 - lce_peak / mpeak, 4),
@@ -267,7 +300,8 @@ def main():
         "config": {"workload": args.workload if args.dtype is None else f"{args.workload}_{args.dtype}",
                    "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
-        "roofline": roofline, "forward_only": forward_only, "rmsnorm_fused": rmsnorm, "memory": memory,
+        "roofline": roofline, "forward_only": forward_only, "rmsnorm_fused": rmsnorm, "head_train_step": head,
+        "memory": memory,
     }
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host cores ...")

@@ -168,6 +168,55 @@ lce_status_t lce_host_adam_step(float* param, const void* grad, int dtype, float
                                 int64_t step, void* param16, int n_threads);
 
 /*
+ * One training step of the output layer with its FP32 master weights, Adam states and 16-bit
+ * gradient/parameter buffers in host memory: the layer-sliding schedule of Section 3.1
+ * ("Asynchronous Parameter Updating", "Thread-Based Lightweight Engine") and the buffers of
+ * Section 3.2 ("Optimized CPU Memory Layout with Shared Buffers", "Layer-Adam Optimizer"), applied
+ * to blocks of vocabulary rows of this one layer.
+ *
+ * On `stream`: lce_forward_backward on `weight`, with the last chunk's dW contraction run as
+ * `vocab_blocks` launches over consecutive row blocks. With overlap = 1, each block's gradient is
+ * copied into grad_host on a side stream as soon as it is computed; the calling thread updates that
+ * block (lce_host_adam_step with n_threads threads, writing the 16-bit result into param_host) as
+ * soon as its copy has landed, and copies it back into `weight` on a second side stream (after the
+ * last dH contraction, the last reader of `weight`). With overlap = 0 the same work runs one phase
+ * after the other (all copies out, the whole update, all copies in) as a reference schedule; both
+ * give bitwise identical results.
+ *
+ *   hidden, labels, N, H, V, dtype (BF16 or FP16; FP32 gives LCE_ERR_UNSUPPORTED), ignore_index,
+ *   reduction (MEAN/SUM), chunk_tokens, workspace: as for lce_forward_backward.
+ *   weight      : device [V,H] dtype: this step's weights; updated in place (rounded from master).
+ *   grad_hidden : device [N,H] dtype (dH, as in lce_forward_backward); loss: device fp32 [1].
+ *   grad_weight : device [V,H] dtype: receives this step's dW.
+ *   master, exp_avg, exp_avg_sq: HOST fp32 [V,H], updated in place (AdamW, see lce_host_adam_step).
+ *   grad_host, param_host: HOST [V,H] dtype, pinned for asynchronous copies (page-locked memory from
+ *                 hipHostMalloc); receive dW and the rounded updated weights.
+ *   step        : Adam step count (>= 1); vocab_blocks in [1, 256].
+ *   timing      : optional; receives the phases of this call (milliseconds).
+ * Unlike the other entry points this call synchronises: it returns when the update and the copies
+ * are complete (and `stream` is ordered after them). It creates and destroys two non-blocking
+ * streams and its events per call; it allocates no memory. Errors as for lce_forward_backward and
+ * lce_host_adam_step; LCE_ERR_HIP if a copy or stream operation fails.
+ */
+typedef struct {
+  double step_ms;    /* wall time of the call                                               */
+  double gpu_ms;     /* the forward + backward contractions on `stream`                     */
+  double d2h_ms;     /* sum over blocks of the gradient copies                              */
+  double update_ms;  /* host time inside the optimizer                                      */
+  double h2d_ms;     /* sum over blocks of the parameter copies                             */
+  double tail_ms;    /* from the end of the GPU work to the end of the last parameter copy  */
+} lce_head_step_timing_t;
+lce_status_t lce_head_train_step(const void* hidden, const int64_t* labels, int64_t N, int64_t H,
+                                 int64_t V, int dtype, int64_t ignore_index, int reduction,
+                                 int64_t chunk_tokens, void* weight, void* grad_hidden,
+                                 void* grad_weight, float* loss, float* master, float* exp_avg,
+                                 float* exp_avg_sq, void* grad_host, void* param_host,
+                                 const lce_adam_config_t* adam, int64_t step, int vocab_blocks,
+                                 int n_threads, int overlap, void* workspace,
+                                 size_t workspace_bytes, void* stream,
+                                 lce_head_step_timing_t* timing);
+
+/*
  * Per-kernel timing, for measurement tools (not for concurrent use). While enabled, every launch of
  * lce_forward / lce_forward_backward (and of their RMSNorm variants) is bracketed by two hipEvents
  * recorded on the call's stream.

@@ -13,6 +13,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cstdint>
 #include <cstring>
 #include <mutex>
@@ -192,10 +193,21 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Optional events for a caller that streams dW out as it is produced: the last chunk's dW GEMM runs
+// as `blocks` launches over consecutive ranges of vocabulary rows (multiples of the tile), each
+// followed by dw_done[b]; dh_done is recorded after the last chunk's dH (W is not read after it).
+struct DwBlocks {
+  int blocks = 0;
+  hipEvent_t* dw_done = nullptr;
+  int64_t* row0 = nullptr;     // [blocks + 1] row boundaries, filled by run
+  hipEvent_t dh_done = nullptr;
+};
+
 // dx32 (optional): receives d loss / d hidden in fp32 instead of dH (the plan must have dx_f32).
 template <typename T>
 lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_t ignore_index, int reduction,
-                 float* loss, float* lse_user, T* dH, T* dW, char* ws, hipStream_t s, float* dx32 = nullptr) {
+                 float* loss, float* lse_user, T* dH, T* dW, char* ws, hipStream_t s, float* dx32 = nullptr,
+                 DwBlocks* hook = nullptr) {
   const int64_t N = p.N, H = p.H, V = p.V;
   int* nvalid = (int*)(ws + p.o_nvalid);
   float* tgt = (float*)(ws + p.o_tgt);
@@ -294,7 +306,26 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     gw.out = dW; gw.ldo = H;
     gw.mode = c == 0 ? DW_STORE : DW_ACCUMULATE;
     gw.n_valid = nvalid; gw.mean = mean;
-    {
+    const bool last = c == p.chunks - 1;
+    if (hook && last) {
+      if (hipEventRecord(hook->dh_done, s) != hipSuccess) return LCE_ERR_HIP;
+      const int64_t tiles = cdiv(V, kTile);
+      for (int b = 0; b < hook->blocks; ++b) {
+        const int64_t r0 = std::min(V, tiles * b / hook->blocks * kTile);
+        const int64_t r1 = std::min(V, tiles * (b + 1) / hook->blocks * kTile);
+        hook->row0[b] = r0;
+        hook->row0[b + 1] = r1;
+        if (r1 > r0) {
+          GemmArgs gb = gw;
+          gb.A = ez + r0;               // MN-contiguous over the vocabulary: rows r0.. of dZ^T
+          gb.M = (int)(r1 - r0);
+          gb.out = dW + r0 * H;
+          KernelTimer t(T_DW, s);
+          if (launch_gemm<T, EPI_DW, true, true>(gb, s) != hipSuccess) return LCE_ERR_HIP;
+        }
+        if (hipEventRecord(hook->dw_done[b], s) != hipSuccess) return LCE_ERR_HIP;
+      }
+    } else {
     KernelTimer t(T_DW, s);
     if (launch_gemm<T, EPI_DW, true, true>(gw, s) != hipSuccess) return LCE_ERR_HIP;
     }
@@ -367,6 +398,133 @@ lce_status_t run_rms(const RmsPlan& rp, const T* h, const T* gamma, const T* W, 
   hipLaunchKernelGGL((rmsnorm_gamma_reduce_kernel<T>), dim3((unsigned)cdiv(H, 256)), dim3(256), 0, s,
                      (const float*)part, (int)rp.row_blocks, H, dgamma);
   return hipGetLastError() == hipSuccess ? LCE_OK : LCE_ERR_HIP;
+}
+
+// ---- one training step of the output layer with its weights kept in host memory ----
+//
+// Section 3.1 ("Asynchronous Parameter Updating"): once a layer's backward finishes, its gradient
+// goes d2h on a side stream while the CPU updates the previous piece and the GPU keeps computing;
+// Section 3.2: FP32 masters in host memory, gradients in a pinned 16-bit buffer, the updated
+// parameters converted to 16 bits in a pinned buffer before the h2d copy. For the output layer
+// alone the pieces are blocks of vocabulary rows: the last chunk's dW GEMM runs block by block, each
+// block's gradient is copied out as soon as it is done, the host updates it while later blocks are
+// still being computed or copied, and the updated block is copied back on a second side stream.
+struct StepClock {
+  hipEvent_t a = nullptr, b = nullptr;
+  bool ok() const { return a && b; }
+};
+
+double event_ms(hipEvent_t a, hipEvent_t b) {
+  float ms = 0.f;
+  return hipEventElapsedTime(&ms, a, b) == hipSuccess ? (double)ms : 0.0;
+}
+
+template <typename T>
+lce_status_t run_head(const Plan& p, const T* X, const int64_t* y, int64_t ignore_index, int reduction,
+                      T* W, T* dH, T* dW, float* loss, float* master, float* m, float* v, T* grad_host,
+                      T* param_host, const lce_adam_config_t* adam, int64_t step, int blocks, int threads,
+                      bool overlap, char* ws, hipStream_t s, lce_head_step_timing_t* timing) {
+  const auto t_start = std::chrono::steady_clock::now();
+  const int64_t H = p.H, V = p.V;
+  const int dt = std::is_same<T, bf16>::value ? LCE_DTYPE_BF16 : LCE_DTYPE_FP16;
+  hipStream_t sd = nullptr, su = nullptr;
+  std::vector<hipEvent_t> evs;
+  auto ev = [&]() -> hipEvent_t {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    evs.push_back(e);
+    return e;
+  };
+  lce_status_t st = LCE_OK;
+  double update_ms = 0.0;
+  std::vector<hipEvent_t> dw_done(blocks), d2h_a(blocks), d2h_b(blocks), h2d_a(blocks), h2d_b(blocks);
+  std::vector<int64_t> row0(blocks + 1, 0);
+  hipEvent_t g0 = nullptr, g1 = nullptr, dh_done = nullptr, upd_end = nullptr;
+  do {
+    if (hipStreamCreateWithFlags(&sd, hipStreamNonBlocking) != hipSuccess ||
+        hipStreamCreateWithFlags(&su, hipStreamNonBlocking) != hipSuccess) { st = LCE_ERR_HIP; break; }
+    g0 = ev(); g1 = ev(); dh_done = ev(); upd_end = ev();
+    for (int b = 0; b < blocks; ++b) {
+      dw_done[b] = ev(); d2h_a[b] = ev(); d2h_b[b] = ev(); h2d_a[b] = ev(); h2d_b[b] = ev();
+    }
+    if (!g0 || !g1 || !dh_done || !upd_end || !h2d_b[blocks - 1]) { st = LCE_ERR_HIP; break; }
+    if (hipEventRecord(g0, s) != hipSuccess) { st = LCE_ERR_HIP; break; }
+    DwBlocks hook;
+    hook.blocks = blocks;
+    hook.dw_done = dw_done.data();
+    hook.row0 = row0.data();
+    hook.dh_done = dh_done;
+    st = run<T>(p, X, W, y, ignore_index, reduction, loss, nullptr, dH, dW, ws, s, nullptr, &hook);
+    if (st != LCE_OK) break;
+    if (hipEventRecord(g1, s) != hipSuccess) { st = LCE_ERR_HIP; break; }
+    if (!overlap) {
+      // Sequential reference schedule: all of the step, then all copies and the whole update.
+      if (hipStreamWaitEvent(sd, g1, 0) != hipSuccess || hipStreamWaitEvent(su, g1, 0) != hipSuccess) {
+        st = LCE_ERR_HIP; break;
+      }
+    } else if (hipStreamWaitEvent(su, dh_done, 0) != hipSuccess) {  // W is free once the last dH is done
+      st = LCE_ERR_HIP; break;
+    }
+    // Gradient blocks out, in order, each as soon as its GEMM block is done.
+    for (int b = 0; b < blocks && st == LCE_OK; ++b) {
+      const size_t off = (size_t)row0[b] * H, n = (size_t)(row0[b + 1] - row0[b]) * H;
+      if ((overlap && hipStreamWaitEvent(sd, dw_done[b], 0) != hipSuccess) || hipEventRecord(d2h_a[b], sd) != hipSuccess ||
+          (n && hipMemcpyAsync(grad_host + off, dW + off, n * sizeof(T), hipMemcpyDeviceToHost, sd) != hipSuccess) ||
+          hipEventRecord(d2h_b[b], sd) != hipSuccess)
+        st = LCE_ERR_HIP;
+    }
+    if (st != LCE_OK) break;
+    // Sequential schedule: every gradient block is in host memory before the update starts.
+    if (!overlap && hipStreamSynchronize(sd) != hipSuccess) { st = LCE_ERR_HIP; break; }
+    // Host update of each block when its gradient has landed, then its parameters back in (the
+    // sequential schedule holds the copies back until the whole update is done).
+    for (int b = 0; b < blocks && st == LCE_OK; ++b) {
+      const size_t off = (size_t)row0[b] * H, n = (size_t)(row0[b + 1] - row0[b]) * H;
+      if (hipEventSynchronize(d2h_b[b]) != hipSuccess) { st = LCE_ERR_HIP; break; }
+      const auto u0 = std::chrono::steady_clock::now();
+      if (n) st = lce_host_adam_step(master + off, grad_host + off, dt, m + off, v + off, (int64_t)n, adam, step,
+                                     param_host + off, threads);
+      update_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - u0).count();
+      if (st != LCE_OK) break;
+      if (!overlap) continue;
+      if (hipEventRecord(h2d_a[b], su) != hipSuccess ||
+          (n && hipMemcpyAsync(W + off, param_host + off, n * sizeof(T), hipMemcpyHostToDevice, su) != hipSuccess) ||
+          hipEventRecord(h2d_b[b], su) != hipSuccess)
+        st = LCE_ERR_HIP;
+    }
+    for (int b = 0; b < blocks && st == LCE_OK && !overlap; ++b) {
+      const size_t off = (size_t)row0[b] * H, n = (size_t)(row0[b + 1] - row0[b]) * H;
+      if (hipEventRecord(h2d_a[b], su) != hipSuccess ||
+          (n && hipMemcpyAsync(W + off, param_host + off, n * sizeof(T), hipMemcpyHostToDevice, su) != hipSuccess) ||
+          hipEventRecord(h2d_b[b], su) != hipSuccess)
+        st = LCE_ERR_HIP;
+    }
+    if (st != LCE_OK) break;
+    // The caller's stream sees the updated weights; the call returns when everything is done.
+    if (hipEventRecord(upd_end, su) != hipSuccess || hipStreamWaitEvent(s, upd_end, 0) != hipSuccess ||
+        hipStreamSynchronize(su) != hipSuccess || hipStreamSynchronize(sd) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      st = LCE_ERR_HIP;
+  } while (false);
+  if (st == LCE_OK && timing) {
+    timing->step_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    timing->gpu_ms = event_ms(g0, g1);
+    timing->d2h_ms = timing->h2d_ms = 0.0;
+    for (int b = 0; b < blocks; ++b) {
+      timing->d2h_ms += event_ms(d2h_a[b], d2h_b[b]);
+      timing->h2d_ms += event_ms(h2d_a[b], h2d_b[b]);
+    }
+    timing->update_ms = update_ms;
+    timing->tail_ms = event_ms(g1, upd_end);
+  }
+  if (st != LCE_OK) {  // leave no work behind on the side streams before releasing them
+    if (sd) (void)hipStreamSynchronize(sd);
+    if (su) (void)hipStreamSynchronize(su);
+  }
+  for (auto e : evs) (void)hipEventDestroy(e);
+  if (sd) (void)hipStreamDestroy(sd);
+  if (su) (void)hipStreamDestroy(su);
+  return st;
 }
 
 }  // namespace
@@ -489,6 +647,41 @@ lce_status_t lce_rmsnorm_forward_backward(const void* hidden, const void* gamma,
   return lce::run_rms<float>(rp, (const float*)hidden, (const float*)gamma, (const float*)weight, labels, eps,
                              ignore_index, reduction, loss, nullptr, nullptr, (float*)grad_hidden,
                              (float*)grad_gamma, (float*)grad_weight, ws, s);
+}
+
+lce_status_t lce_head_train_step(const void* hidden, const int64_t* labels, int64_t N, int64_t H, int64_t V,
+                                 int dtype, int64_t ignore_index, int reduction, int64_t chunk_tokens,
+                                 void* weight, void* grad_hidden, void* grad_weight, float* loss, float* master,
+                                 float* exp_avg, float* exp_avg_sq, void* grad_host, void* param_host,
+                                 const lce_adam_config_t* adam, int64_t step, int vocab_blocks, int n_threads,
+                                 int overlap, void* workspace, size_t workspace_bytes, void* stream,
+                                 lce_head_step_timing_t* timing) {
+  if (!hidden || !labels || !weight || !grad_hidden || !grad_weight || !loss || !master || !exp_avg ||
+      !exp_avg_sq || !grad_host || !param_host || !adam || step < 1 || vocab_blocks < 1 || vocab_blocks > 256 ||
+      n_threads < 0)
+    return LCE_ERR_INVALID_ARGUMENT;
+  if (reduction != LCE_REDUCTION_MEAN && reduction != LCE_REDUCTION_SUM) return LCE_ERR_INVALID_ARGUMENT;
+  if (dtype != LCE_DTYPE_BF16 && dtype != LCE_DTYPE_FP16) return dtype == LCE_DTYPE_FP32 ? LCE_ERR_UNSUPPORTED
+                                                                                        : LCE_ERR_INVALID_ARGUMENT;
+  lce::Plan p;
+  lce_status_t st = lce::make_plan(N, H, V, dtype, true, chunk_tokens, p, true);
+  if (st != LCE_OK) return st;
+  if (!workspace || workspace_bytes < p.total) return LCE_ERR_WORKSPACE_TOO_SMALL;
+  // The optimizer settings are checked before any GPU work.
+  const lce_adam_config_t& a = *adam;
+  if (!(a.lr >= 0.f && a.lr < 3.0e38f) || !(a.beta1 >= 0.f && a.beta1 < 1.f) || !(a.beta2 >= 0.f && a.beta2 < 1.f) ||
+      !(a.eps > 0.f && a.eps < 3.0e38f) || !(a.weight_decay >= 0.f && a.weight_decay < 3.0e38f))
+    return LCE_ERR_INVALID_ARGUMENT;
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LCE_DTYPE_BF16)
+    return lce::run_head<lce::bf16>(p, (const lce::bf16*)hidden, labels, ignore_index, reduction, (lce::bf16*)weight,
+                                    (lce::bf16*)grad_hidden, (lce::bf16*)grad_weight, loss, master, exp_avg, exp_avg_sq,
+                                    (lce::bf16*)grad_host, (lce::bf16*)param_host, adam, step, vocab_blocks,
+                                    n_threads, overlap != 0, (char*)workspace, s, timing);
+  return lce::run_head<lce::f16>(p, (const lce::f16*)hidden, labels, ignore_index, reduction, (lce::f16*)weight,
+                                 (lce::f16*)grad_hidden, (lce::f16*)grad_weight, loss, master, exp_avg, exp_avg_sq,
+                                 (lce::f16*)grad_host, (lce::f16*)param_host, adam, step, vocab_blocks, n_threads,
+                                 overlap != 0, (char*)workspace, s, timing);
 }
 
 lce_status_t lce_timing_enable(int enable) {

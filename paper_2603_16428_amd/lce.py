@@ -22,11 +22,20 @@ DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
 EXPORTED = ("lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
             "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward", "lce_rmsnorm_forward_backward",
-            "lce_host_adam_step",
+            "lce_host_adam_step", "lce_head_train_step",
             "lce_timing_enable", "lce_timing_read", "lce_status_string")
 TIMING_KINDS = ("logits_lse_gemm", "dh_gemm", "dw_gemm", "dlogits", "transpose", "other")
 
 _lib = None
+
+
+class HeadStepTiming(ctypes.Structure):
+    """lce_head_step_timing_t (milliseconds)."""
+    _fields_ = [("step_ms", ctypes.c_double), ("gpu_ms", ctypes.c_double), ("d2h_ms", ctypes.c_double),
+                ("update_ms", ctypes.c_double), ("h2d_ms", ctypes.c_double), ("tail_ms", ctypes.c_double)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 class AdamConfig(ctypes.Structure):
@@ -71,6 +80,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.lce_host_adam_step.argtypes = [vp, vp, ctypes.c_int, vp, vp, i64, ctypes.POINTER(AdamConfig), i64, vp,
                                        ctypes.c_int]
     lib.lce_host_adam_step.restype = ctypes.c_int
+    lib.lce_head_train_step.argtypes = [vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, i64, vp, vp, vp,
+                                        vp, vp, vp, vp, vp, vp, ctypes.POINTER(AdamConfig), i64, ctypes.c_int,
+                                        ctypes.c_int, ctypes.c_int, vp, sz, vp, ctypes.POINTER(HeadStepTiming)]
+    lib.lce_head_train_step.restype = ctypes.c_int
     lib.lce_timing_enable.argtypes = [ctypes.c_int]
     lib.lce_timing_enable.restype = ctypes.c_int
     lib.lce_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
@@ -324,3 +337,57 @@ def host_adam_step(param, grad, exp_avg, exp_avg_sq, step: int, lr: float, betas
                                 ctypes.byref(cfg), step, _ptr(param16), threads)
     if st != LCE_OK:
         raise LCEError(st, "lce_host_adam_step")
+
+
+# ---- a training step of the output layer with host-resident weights -------------------------------
+
+class HeadState:
+    """Host and device buffers of the output layer for lce_head_train_step.
+
+    The FP32 master copy and the Adam states live in host memory; the 16-bit gradient and parameter
+    buffers are pinned (torch's pin_memory allocates page-locked memory); `weight` is the device copy
+    the step reads and refreshes.
+    """
+
+    def __init__(self, weight: torch.Tensor):
+        if weight.dtype not in (torch.bfloat16, torch.float16) or not weight.is_cuda:
+            raise ValueError("weight must be a bf16 or fp16 device tensor")
+        self.weight = weight
+        self.master = weight.detach().float().cpu()
+        self.exp_avg = torch.zeros_like(self.master)
+        self.exp_avg_sq = torch.zeros_like(self.master)
+        self.grad_host = torch.empty(weight.shape, dtype=weight.dtype, pin_memory=True)
+        self.param_host = torch.empty(weight.shape, dtype=weight.dtype, pin_memory=True)
+        self.grad_weight = torch.empty_like(weight)
+        self.step = 0
+
+
+def head_train_step(state: HeadState, hidden, labels, lr: float, betas=(0.9, 0.999), eps: float = 1e-8,
+                    weight_decay: float = 0.0, ignore_index: int = -100, reduction: str = "mean",
+                    chunk_tokens: int = 0, vocab_blocks: int = 8, threads: int = 0, overlap: bool = True,
+                    workspace: torch.Tensor | None = None):
+    """One step: loss and dH on the device, W updated through the host; returns (loss, dH, timing)."""
+    lib = load_library()
+    W = state.weight
+    N, H, V = _check_inputs(hidden, W, labels)
+    dt = DTYPES[hidden.dtype]
+    red = REDUCTIONS[reduction]
+    need = lib.lce_workspace_size(N, H, V, dt, 1, chunk_tokens)
+    if need == 0:
+        raise LCEError(2, "lce_workspace_size")
+    ws = workspace if workspace is not None else _workspace(need, hidden.device)
+    loss = torch.empty(1, dtype=torch.float32, device=hidden.device)
+    dH = torch.empty_like(hidden)
+    state.step += 1
+    cfg = AdamConfig(lr, betas[0], betas[1], eps, weight_decay)
+    timing = HeadStepTiming()
+    stream = ctypes.c_void_p(torch.cuda.current_stream(hidden.device).cuda_stream)
+    st = lib.lce_head_train_step(_ptr(hidden), _ptr(labels), N, H, V, dt, ignore_index, red, chunk_tokens, _ptr(W),
+                                 _ptr(dH), _ptr(state.grad_weight), _ptr(loss), _ptr(state.master),
+                                 _ptr(state.exp_avg), _ptr(state.exp_avg_sq), _ptr(state.grad_host),
+                                 _ptr(state.param_host), ctypes.byref(cfg), state.step, vocab_blocks, threads,
+                                 int(overlap), _ptr(ws), ws.numel(), stream, ctypes.byref(timing))
+    if st != LCE_OK:
+        state.step -= 1
+        raise LCEError(st, "lce_head_train_step")
+    return loss[0], dH, timing.as_dict()

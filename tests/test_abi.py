@@ -32,7 +32,8 @@ def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward",
                             "lce_forward_backward", "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward",
-                            "lce_rmsnorm_forward_backward", "lce_host_adam_step", "lce_timing_enable",
+                            "lce_rmsnorm_forward_backward", "lce_host_adam_step", "lce_head_train_step",
+                            "lce_timing_enable",
                             "lce_timing_read", "lce_status_string"])
     for n in names:
         assert hasattr(lib, n), n
@@ -161,3 +162,34 @@ def test_rmsnorm_forward_validation(lib, kw, status):
 ])
 def test_rmsnorm_forward_backward_validation(lib, kw, status):
     assert _rfb(lib, **kw) == status
+
+
+# ---- the output-layer training step ---------------------------------------------------------------
+
+def _head(lib, **kw):
+    from paper_2603_16428_amd import lce as L
+    cfg = kw.pop("cfg", L.AdamConfig(1e-3, 0.9, 0.999, 1e-8, 0.0))
+    a = dict(hidden=FAKE, labels=FAKE, N=16, H=64, V=100, dtype=BF16, ignore=-100, red=MEAN, chunk=0, w=FAKE,
+             dh=FAKE, dw=FAKE, loss=FAKE, master=FAKE, m=FAKE, v=FAKE, gh=FAKE, ph=FAKE, step=1, blocks=4,
+             threads=0, overlap=1, ws=FAKE, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return lib.lce_head_train_step(a["hidden"], a["labels"], a["N"], a["H"], a["V"], a["dtype"], a["ignore"],
+                                   a["red"], a["chunk"], a["w"], a["dh"], a["dw"], a["loss"], a["master"], a["m"],
+                                   a["v"], a["gh"], a["ph"], ctypes.byref(cfg), a["step"], a["blocks"], a["threads"],
+                                   a["overlap"], a["ws"], a["wsb"], a["stream"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(master=None), INVALID), (dict(gh=None), INVALID), (dict(ph=None), INVALID), (dict(step=0), INVALID),
+    (dict(blocks=0), INVALID), (dict(blocks=257), INVALID), (dict(threads=-1), INVALID), (dict(red=NONE), INVALID),
+    (dict(dtype=FP32), UNSUPPORTED), (dict(dtype=9), INVALID), (dict(H=60), UNSUPPORTED), (dict(wsb=8), WS_SMALL),
+])
+def test_head_train_step_validation(lib, kw, status):
+    assert _head(lib, **kw) == status
+
+
+def test_head_train_step_rejects_bad_optimizer_settings(lib):
+    from paper_2603_16428_amd import lce as L
+    for cfg in (L.AdamConfig(-1e-3, 0.9, 0.999, 1e-8, 0.0), L.AdamConfig(1e-3, 1.0, 0.999, 1e-8, 0.0),
+                L.AdamConfig(1e-3, 0.9, 0.999, 0.0, 0.0), L.AdamConfig(1e-3, 0.9, 0.999, 1e-8, -0.5)):
+        assert _head(lib, cfg=cfg) == INVALID
