@@ -67,3 +67,18 @@ def forward(hidden, gamma, weight, labels, eps: float = 1e-5, ignore_index: int 
     out = lce.forward(x, weight, labels, ignore_index, reduction)
     out["x"], out["r"] = x, r
     return out
+
+
+def grad_hidden_rows(hidden, gamma, weight, labels, rows, g, eps: float = 1e-5, ignore_index: int = -100):
+    """d h_i for the listed tokens only (their dX rows from ``lce.grad_hidden_rows``, then the
+    chain rule above); ``g`` are the token weights of ``lce.token_weights``."""
+    h = lce._as_f64(hidden)
+    gm = lce._as_f64(gamma)
+    rows = np.asarray(rows, dtype=np.int64)
+    x, r = rms_normalise(h[rows], gm, eps)
+    xs = np.zeros_like(h)
+    xs[rows] = x
+    dX = lce.grad_hidden_rows(xs, weight, labels, rows, g, ignore_index)
+    hr = h[rows]
+    s = np.sum(hr * gm[None, :] * dX, axis=1)
+    return r[:, None] * gm[None, :] * dX - (r ** 3)[:, None] * hr * (s / h.shape[1])[:, None]
