@@ -4,10 +4,11 @@
 // token chunks, the N x V logits never held):
 //   count valid labels (global mean divisor) -> target logits
 //   for each chunk of n_c tokens:
+//     fragment-blocked copies of X_c (operand B of the logits and dW GEMMs)
 //     logits^T tile GEMM with the log-sum-exp epilogue  (stores e = exp(z - m_slice) for backward)
 //     row combine -> lse, token losses
-//     [backward] dlogits in place -> dH rows GEMM (reads W as it is) -> dW GEMM (reads dZ and X
-//                as they are; the first chunk writes dW, later chunks add to it)
+//     [backward] dlogits in place -> dH rows GEMM (reads W as it is) -> dW GEMM (reads dZ as it
+//                is; the first chunk writes dW, later chunks add to it)
 //   loss reduction (fp64, fixed order)
 #include <hip/hip_runtime.h>
 
@@ -79,8 +80,12 @@ struct Plan {
   int64_t slices = 0;
   int dh_splits = 1;
   int64_t dh_kps = 0;             // K (vocabulary) per dH split, multiple of the K-tile
+  // Fragment-blocked copies of a chunk's X: operand B of the logits GEMM (columns = tokens,
+  // K = H) and of the dW GEMM (columns = H, K = tokens): column blocks and K-pairs per block.
+  int64_t xk_nb = 0, xk_kp = 0, xm_nb = 0, xm_kp = 0;
   // workspace offsets (bytes)
   size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_dhp = 0;
+  size_t o_xk = 0, o_xm = 0;
   size_t total = 0;
 };
 
@@ -131,6 +136,11 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   const int64_t maxpitch = std::max({H, p.Vp});
   if ((int64_t)kTile * maxpitch * p.esz > lim || N > lim / 2 || V > lim / 2 || H > lim / 2) return LCE_ERR_UNSUPPORTED;
   if (cdiv(V, kTile) * cdiv(H, kTile) > lim / 16 || cdiv(p.ncp * p.Vp, 2048) > lim) return LCE_ERR_UNSUPPORTED;
+  p.xk_nb = cdiv(p.ncp, 32);
+  p.xk_kp = round_up(H * p.esz, kTileBytes) / 32;
+  p.xm_nb = cdiv(H, 32);
+  p.xm_kp = round_up(p.ncp * p.esz, kTileBytes) / 32;
+  if (p.xk_nb * p.xk_kp * 1024 > lim || p.xm_nb * p.xm_kp * 1024 > lim) return LCE_ERR_UNSUPPORTED;
 
   if (backward) {
     // dH tiles of one chunk: split the vocabulary (K) so that the grid fills the device.
@@ -162,7 +172,9 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.o_tl = take((size_t)N * 4);
   p.o_pmax = take((size_t)p.slices * p.ncp * 4);
   p.o_psum = take((size_t)p.slices * p.ncp * 4);
+  p.o_xk = take((size_t)(p.xk_nb * p.xk_kp * 1024));
   if (backward) {
+    p.o_xm = take((size_t)(p.xm_nb * p.xm_kp * 1024));
     p.o_e = take((size_t)p.ncp * p.Vp * p.esz);
     if (p.dh_splits > 1 || dx_f32) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
   }
@@ -170,8 +182,14 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   return LCE_OK;
 }
 
-template <typename T, int EPI, bool A_MN, bool B_MN>
+// KCHECK: a K-contig operand's K range may end inside a K-tile and its rows are not zero-padded
+// up to the next one (see Operand::offset). XB: operand B is a fragment-blocked copy, read by
+// gemm_xb_kernel (B_MN is then ignored).
+template <typename T, int EPI, bool A_MN, bool B_MN, bool KCHECK = false, bool XB = false>
 hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
+  const void* fn = XB ? (const void*)gemm_xb_kernel<T, EPI, A_MN, KCHECK>
+                      : (const void*)gemm_kernel<T, EPI, A_MN, B_MN, KCHECK>;
+  const int smem = XB ? kXbSmem : kGemmSmem;
   static std::atomic<uint64_t> configured[kMaxDevices / 64 + 1];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -179,8 +197,7 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   if (dev < kMaxDevices) {
     const uint64_t bit = uint64_t(1) << (dev & 63);
     if (!(configured[dev >> 6].load() & bit)) {
-      e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI, A_MN, B_MN>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              kGemmSmem);
+      e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
       if (e != hipSuccess) return e;
       configured[dev >> 6].fetch_or(bit);
     }
@@ -189,7 +206,11 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   g.tiles_n = (int)cdiv(g.N, kTile);
   const int blocks = g.tiles_m * g.tiles_n * g.splits;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<T, EPI, A_MN, B_MN>), dim3(blocks), dim3(kGemmThreads), kGemmSmem, s, g);
+  if constexpr (XB) {
+    hipLaunchKernelGGL((gemm_xb_kernel<T, EPI, A_MN, KCHECK>), dim3(blocks), dim3(kGemmThreads), smem, s, g);
+  } else {
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, A_MN, B_MN, KCHECK>), dim3(blocks), dim3(kGemmThreads), smem, s, g);
+  }
   return hipGetLastError();
 }
 
@@ -216,6 +237,8 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
   float* pmax = (float*)(ws + p.o_pmax);
   float* psum = (float*)(ws + p.o_psum);
   T* ez = p.backward ? (T*)(ws + p.o_e) : nullptr;
+  T* xk = (T*)(ws + p.o_xk);
+  T* xm = p.backward ? (T*)(ws + p.o_xm) : nullptr;
   float* dhp = (p.backward && (p.dh_splits > 1 || dx32)) ? (float*)(ws + p.o_dhp) : nullptr;
   const int mean = reduction == LCE_REDUCTION_MEAN;
 
@@ -231,10 +254,21 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     const int64_t t0 = c * p.nc;
     const int rows = (int)std::min(p.nc, N - t0);
 
+    // Fragment-blocked copies of X_c: operand B of the logits GEMM and, backward, of the dW GEMM.
+    {
+    KernelTimer t(T_OTHER, s);
+    hipLaunchKernelGGL((block_k_kernel<T>), dim3((unsigned)cdiv(p.xk_nb * p.xk_kp * 64, 256)), dim3(256), 0, s,
+                       X + t0 * H, H, rows, (int)H, (int)p.xk_kp, (int)p.xk_nb, xk);
+    if (p.backward)
+      hipLaunchKernelGGL((block_mn_kernel<T>), dim3((unsigned)p.xm_nb, (unsigned)cdiv(p.xm_kp, 4)), dim3(256), 0, s,
+                         X + t0 * H, H, (int)H, rows, (int)p.xm_kp, xm);
+    }
+    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+
     // logits^T tile = W . X_c^T with the log-sum-exp epilogue.
     GemmArgs g{};
     g.A = W; g.lda = H; g.M = (int)V;
-    g.B = X + t0 * H; g.ldb = H; g.N = rows;
+    g.B = xk; g.ldb = p.xk_kp; g.N = rows;
     g.K = (int)H;
     g.splits = 1; g.k_per_split = (int)round_up(H, kTileBytes / p.esz);
     g.group_m = 4;
@@ -242,11 +276,15 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     hipError_t e;
     {
     KernelTimer t(T_LOGITS, s);
+    // W's rows end at H: whole K-tiles read them unchecked only when H is made of whole K-tiles.
+    const bool whole = H % (kTileBytes / p.esz) == 0;
     if (p.backward) {
       g.out = ez; g.ldo = p.Vp;
-      e = launch_gemm<T, EPI_LSE_BWD, false, false>(g, s);
+      e = whole ? launch_gemm<T, EPI_LSE_BWD, false, false, false, true>(g, s)
+                : launch_gemm<T, EPI_LSE_BWD, false, false, true, true>(g, s);
     } else {
-      e = launch_gemm<T, EPI_LSE_FWD, false, false>(g, s);
+      e = whole ? launch_gemm<T, EPI_LSE_FWD, false, false, false, true>(g, s)
+                : launch_gemm<T, EPI_LSE_FWD, false, false, true, true>(g, s);
     }
     }
     if (e != hipSuccess) return LCE_ERR_HIP;
@@ -267,7 +305,8 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
     }
 
-    // dH rows of the chunk = dZ_c . W  (A = dZ_c [rows, Vp] K-contig, B = W [V, H] MN-contig).
+    // dH rows of the chunk = dZ_c . W  (A = dZ_c [rows, Vp] K-contig, B = W [V, H] MN-contig). dZ's
+    // rows are zero-padded to Vp, a multiple of every K-tile, so its loads read whole K-tiles.
     GemmArgs gh{};
     gh.A = ez; gh.lda = p.Vp; gh.M = rows;
     gh.B = W; gh.ldb = H; gh.N = (int)H;
@@ -296,10 +335,10 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     }
     }
 
-    // dW (+)= dZ_c^T . X_c  (A = dZ_c MN-contig over the vocabulary, B = X_c MN-contig over H).
+    // dW (+)= dZ_c^T . X_c  (A = dZ_c MN-contig over the vocabulary, B = X_c blocked over H).
     GemmArgs gw{};
     gw.A = ez; gw.lda = p.Vp; gw.M = (int)V;
-    gw.B = X + t0 * H; gw.ldb = H; gw.N = (int)H;
+    gw.B = xm; gw.ldb = p.xm_kp; gw.N = (int)H;
     gw.K = rows;
     gw.splits = 1; gw.k_per_split = (int)round_up(rows, kTileBytes / p.esz);
     gw.group_m = 4;
@@ -321,13 +360,13 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
           gb.M = (int)(r1 - r0);
           gb.out = dW + r0 * H;
           KernelTimer t(T_DW, s);
-          if (launch_gemm<T, EPI_DW, true, true>(gb, s) != hipSuccess) return LCE_ERR_HIP;
+          if (launch_gemm<T, EPI_DW, true, true, false, true>(gb, s) != hipSuccess) return LCE_ERR_HIP;
         }
         if (hipEventRecord(hook->dw_done[b], s) != hipSuccess) return LCE_ERR_HIP;
       }
     } else {
     KernelTimer t(T_DW, s);
-    if (launch_gemm<T, EPI_DW, true, true>(gw, s) != hipSuccess) return LCE_ERR_HIP;
+    if (launch_gemm<T, EPI_DW, true, true, false, true>(gw, s) != hipSuccess) return LCE_ERR_HIP;
     }
   }
 

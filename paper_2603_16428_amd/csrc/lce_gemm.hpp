@@ -106,12 +106,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+// voff: per-lane byte offset; soff: uniform byte offset (an SGPR).
+__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff = 0) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, off, 0, 0, 0);
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff, uint32_t soff = 0) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, soff, 0, 0);
 }
 
 __device__ __forceinline__ i16x4 read_tr(const char* lds) {
@@ -224,13 +225,18 @@ __device__ __forceinline__ float dz_epilogue_scale(const int* n_valid, int mean)
 // 24-31, and each store instruction writes 32 contiguous bytes of the row instead of 16 (the
 // stores of a tile's epilogue are a burst that every CU issues at about the same time).
 // in0 / in1: whether this lane's first / second 8 elements lie inside the output.
+// The lane index, recomputed where it is needed: values derived from it early and kept alive
+// through the main loop for the epilogue would be spilled.
+__device__ __forceinline__ int lane_id() {
+  uint32_t ln;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+  return (int)ln;
+}
+
 template <typename T>
 __device__ __forceinline__ void store_row32(T* p, const f32x16& v, bool in0, bool in1) {
   typedef T t4 __attribute__((ext_vector_type(4)));
-  // The lane's half, recomputed here: kept alive from the prologue, the kernel would spill it.
-  uint32_t ln;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
-  const int half = (int)(ln >> 5);
+  const int half = lane_id() >> 5;
   uint32_t a[4], b[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -334,9 +340,30 @@ struct Operand {
     }
   }
 
-  // Byte offset of load j of K-tile t (kOOB where a K-contig chunk lies at or beyond ke). The sum
-  // is formed where it is used: hoisted out of the main loop, the sixteen offsets of two operands
-  // would outgrow the registers and be spilled (and spill traffic would upset the vmcnt waits).
+  // Byte offset of load j of K-tile t, in two parts: a per-lane part, formed by one v_xad_u32 where
+  // it is used (hoisted out of the main loop, the sixteen offsets of two operands would outgrow the
+  // registers and be spilled, and spill traffic would upset the vmcnt waits), and a uniform part in
+  // soffset: j row_step plus, K-contig, the K-tile's start (kOOB for a K-tile at or past ke). A
+  // chain of dependent address instructions in front of each load stalls the in-order issue, and
+  // the MFMAs queued behind it, for tens of cycles per load. K-contig, this reads whole K-tiles:
+  // only for K ranges made of whole K-tiles, or rows whose padding up to the next K-tile is zeros
+  // (or meets zeros in the other operand); otherwise offset() below checks every chunk.
+  __device__ __forceinline__ uint32_t lane_offset(int j) const {
+    uint32_t o;
+    asm volatile("v_xad_u32 %0, %1, %2, %3" : "=v"(o) : "v"(slot_x), "s"(xor_j(j)), "v"(row_off));
+    return o;
+  }
+  __device__ __forceinline__ uint32_t uniform_offset(int t, int j) const {
+    uint32_t o = (uint32_t)j * row_step;
+    if constexpr (!MN) {
+      const int k0 = kb + t * kBK;
+      o = k0 < ke ? o + (uint32_t)k0 * kEsz : kOOB;
+    }
+    return __builtin_amdgcn_readfirstlane(o);
+  }
+
+  // The whole offset with a per-chunk K check (kOOB where a K-contig chunk lies at or beyond ke),
+  // for K-contig operands whose K range ends inside a K-tile.
   __device__ __forceinline__ uint32_t offset(int t, int j) const {
     uint32_t o;
     asm volatile("v_xor_b32 %0, %2, %1\n\tv_add3_u32 %0, %0, %3, %4"
@@ -381,7 +408,171 @@ struct Operand {
   }
 };
 
-template <typename T, int EPI, bool A_MN, bool B_MN>
+// bf16 dW accumulation (chunks after the first): the wave's current dW values in the swapped
+// accumulator layout, loaded raw while the pipeline fills, then the accumulators' starting values.
+__device__ __forceinline__ void load_dw_prev(const GemmArgs& g, bf16x4 (&prev)[4][4][4], int mw, int nw, int lane) {
+  const int sub4 = 4 * (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = mw + 32 * i + (lane & 31);
+    const bf16* o = (const bf16*)g.out + (size_t)row * g.ldo;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = nw + 32 * j + 8 * q + sub4;
+        prev[i][j][q] = (row < g.M && col < g.N) ? *(const bf16x4*)(o + col) : (bf16x4){};
+      }
+  }
+}
+
+__device__ __forceinline__ void apply_dw_prev(f32x16 (&acc)[4][4], const bf16x4 (&prev)[4][4][4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] = (float)prev[i][j][q][e];
+}
+
+// The epilogue: what a wave's 128 x 128 accumulator sub-tile at (mw, nw) becomes. Without the
+// operand swap, accumulator element r of block (i, j) sits at row = 32i + 8(r/4) + 4(l/32) + r%4,
+// col = 32j + l%32 of the sub-tile; with it, at row = 32i + l%32, col = 32j + 8(r/4) + 4(l/32) + r%4.
+// PRELOADED (DW): the accumulators started from the tile's current dW values.
+template <typename T, int EPI, bool PRELOADED>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4][4], int mw, int nw, int split,
+                                              bool accumulate) {
+  constexpr int kEsz = (int)sizeof(T);
+  const int lane = lane_id();
+  const int sub4 = 4 * (lane >> 5);
+  const int l32 = lane & 31;
+  if constexpr (EPI == EPI_LSE_FWD || EPI == EPI_LSE_BWD) {
+    if (mw >= g.M) return;
+    const int slice = mw / kLseSlice;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = nw + 32 * j + l32;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
+          if (row < g.M) mx = fmaxf(mx, acc[i][j][r]);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float ml = mx * kLog2e;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
+          const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
+          s += e;
+          acc[i][j][r] = e * Storage<T>::kE;
+        }
+      s += __shfl_xor(s, 32);
+      if (col < g.N) {
+        if constexpr (EPI == EPI_LSE_BWD) {
+          T* e_row = (T*)g.out + (size_t)col * g.ldo;
+          if constexpr (kEsz == 2) {
+            // Whole 128-row wave slices: e's pitch is M rounded up to 128, and rows at or beyond M
+            // hold exp = 0 here.
+#pragma unroll
+            for (int i = 0; i < 4; ++i) store_row32(e_row + mw + 32 * i, acc[i][j], true, true);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int row = mw + 32 * i + 8 * q + sub4;
+                if (row < g.M)
+                  store4(e_row + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                         acc[i][j][4 * q + 3]);
+              }
+          }
+        }
+        if (lane < 32) {
+          g.pmax[(size_t)slice * g.ldp + col] = mx;
+          g.psum[(size_t)slice * g.ldp + col] = s;
+        }
+      }
+    }
+  } else {
+    // Swapped layout: lane owns rows mw + 32i + l%32 and 4 consecutive columns per (j, q).
+    // N (the output pitch) is a multiple of 4 here, so a 4-column group is all in or all out.
+    const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = mw + 32 * i + l32;
+      if (row >= g.M) continue;
+      if constexpr (EPI == EPI_STORE) {
+        if (g.mode == 1) {
+          float* o = (float*)g.out + (size_t)split * g.M * g.ldo + (size_t)row * g.ldo;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int col = nw + 32 * j + 8 * q + sub4;
+              if (col < g.N)
+                store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+            }
+        } else {
+          T* o = (T*)g.out + (size_t)row * g.ldo;
+          if constexpr (kEsz == 2) {
+            // N is a multiple of 8 for 16-bit types, so an 8-column piece is all in or all out.
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              if constexpr (Storage<T>::kDzUnscaled) acc[i][j] *= sc;
+              const int c0 = nw + 32 * j + 8 * (lane >> 5);
+              store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int col = nw + 32 * j + 8 * q + sub4;
+                if (col < g.N)
+                  store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+              }
+          }
+        }
+      } else if constexpr (PRELOADED) {  // EPI_DW, bf16: the accumulators already hold the earlier chunks' sum
+        T* o = (T*)g.out + (size_t)row * g.ldo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c0 = nw + 32 * j + 8 * (lane >> 5);
+          store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
+        }
+      } else {  // EPI_DW, fp32 and fp16: add the earlier chunks' sum here
+        T* o = (T*)g.out + (size_t)row * g.ldo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          f32x4 base[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            base[q] = (!PRELOADED && accumulate && col < g.N) ? load4(o + col) : (f32x4){};
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            if (col < g.N)
+              store4(o + col, base[q][0] + sc * acc[i][j][4 * q], base[q][1] + sc * acc[i][j][4 * q + 1],
+                     base[q][2] + sc * acc[i][j][4 * q + 2], base[q][3] + sc * acc[i][j][4 * q + 3]);
+          }
+        }
+      }
+    }
+  }
+}
+
+// KCHECK: K-contig operands check every chunk against the K range (see Operand::offset).
+template <typename T, int EPI, bool A_MN, bool B_MN, bool KCHECK>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   constexpr int kEsz = (int)sizeof(T);
@@ -418,7 +609,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     const __amdgpu_buffer_rsrc_t r = opa.rsrc(t);
     char* st = smem + (t % kASlots) * kOperandBytes + w * 8 * 1024;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) dma16(r, st + j * 1024, opa.offset(t, j));
+    for (int j = 0; j < 8; ++j) {
+      if constexpr (KCHECK && !A_MN) dma16(r, st + j * 1024, opa.offset(t, j));
+      else dma16(r, st + j * 1024, opa.lane_offset(j), opa.uniform_offset(t, j));
+    }
   };
   // B K-tile t: into register buffer t % 2 (the caller passes that parity as a constant, so that
   // the buffers stay in registers) ...
@@ -426,7 +620,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   auto load_b = [&](int t, auto par) {
     const __amdgpu_buffer_rsrc_t r = opb.rsrc(t);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) vb[par][j] = load16(r, opb.offset(t, j));
+    for (int j = 0; j < 8; ++j) {
+      if constexpr (KCHECK && !B_MN) vb[par][j] = load16(r, opb.offset(t, j));
+      else vb[par][j] = load16(r, opb.lane_offset(j), opb.uniform_offset(t, j));
+    }
   };
   // ... then from there into LDS slot t % 2, at the same place LDS-DMA would have put it.
   auto write_b = [&](auto par) {
@@ -533,26 +730,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
   // starting values, so the epilogue only stores. (fp32 adds them in the epilogue instead: its
   // 256 values per lane would not fit next to the pipeline's registers.)
   const int mw = m0 + wm * 128, nw = n0 + wn * 128;
-  const int sub4 = 4 * (lane >> 5);
-  const int l32 = lane & 31;
   constexpr bool kPreload = EPI == EPI_DW && std::is_same<T, bf16>::value;
   const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
   bf16x4 prev[kPreload ? 4 : 1][4][4];
   if constexpr (kPreload) {
-    if (accumulate) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = mw + 32 * i + l32;
-        const bf16* o = (const bf16*)g.out + (size_t)row * g.ldo;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int col = nw + 32 * j + 8 * q + sub4;
-            prev[i][j][q] = (row < g.M && col < g.N) ? *(const bf16x4*)(o + col) : (bf16x4){};
-          }
-      }
-    }
+    if (accumulate) load_dw_prev(g, prev, mw, nw, lane);
   }
   // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
   const int nk = (ke - kb + kBK - 1) / kBK;
@@ -562,16 +744,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     load_b(1, P1{});
     load_a(1);
     if constexpr (kPreload) {
-      if (accumulate) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-              for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] = (float)prev[i][j][q][e];
-      }
+      if (accumulate) apply_dw_prev(acc, prev);
     }
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsPerOperand) : "memory");  // B(0) landed
     write_b(P0{});
@@ -589,131 +762,254 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
 
-  // ---- epilogue. Without the swap, accumulator element r of block (i, j) sits at
-  //      row = 32i + 8(r/4) + 4(l/32) + r%4, col = 32j + l%32 of the wave's 128 x 128 sub-tile;
-  //      with it, at row = 32i + l%32, col = 32j + 8(r/4) + 4(l/32) + r%4.
+  gemm_epilogue<T, EPI, kPreload>(g, acc, mw, nw, split, accumulate);
+}
 
-  if constexpr (EPI == EPI_LSE_FWD || EPI == EPI_LSE_BWD) {
-    if (mw >= g.M) return;
-    const int slice = mw / kLseSlice;
+// ---- Operand B straight to registers ---------------------------------------------------------
+//
+// gemm_xb_kernel computes the same tile with the same waves and epilogues, but reads operand B from
+// a fragment-blocked copy straight into the registers the MFMAs take it from: every B load is one
+// whole 1 KB fragment, and B never passes through LDS, which halves a K-tile's LDS traffic (A's
+// 32 KB written, 64 KB read). A streams into a ring of four LDS slots by LDS-DMA, three K-tiles
+// ahead; B circulates through a ring of eight K-pairs of fragments (128 VGPRs), seven K-pairs ahead.
+// A K-tile is four sections of 16 MFMAs; each section issues one quarter of A's K-tile three ahead
+// (two LDS-DMA loads) and the four B fragments of the K-pair seven ahead, between its MFMAs.
+//
+// Blocked layout of B (N columns, reduction K, element type T): fragment (jb, q) -- 32 columns by
+// K-pair q, the q-th 32 bytes of every column's K run -- is 1 KB at byte (jb KP + q) 1024, and lane
+// l of it holds column 32 jb + l%32, bytes [32 q + 16 (l/32), +16): the 16 bytes that lane feeds
+// the MFMA. KP counts the K-pairs per column block with K rounded up to a whole K-tile; columns at
+// or beyond N and K at or beyond K are zeros. (The A fragments read from LDS cover the same K bytes:
+// K-pair p of K-tile t, lane half h, bytes [32 p + 16 h, +16) of the K-tile.)
+constexpr int kXbASlots = 4;
+constexpr int kXbAhead = kXbASlots - 1;
+constexpr int kXbSmem = kXbASlots * kOperandBytes;  // 128 KB
+
+// Blocked copy of a K-contiguous source (element (n, k) at src[n * ld + k]; K a multiple of 16
+// bytes' worth): one thread per 16-byte piece. Grid: NB * KP * 64 threads.
+template <typename T>
+__global__ __launch_bounds__(256) void block_k_kernel(const T* __restrict__ src, int64_t ld, int N, int K, int KP,
+                                                      int NB, T* __restrict__ dst) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t frag = t >> 6;
+  if (frag >= (int64_t)NB * KP) return;
+  const int l = (int)(t & 63);
+  const int jb = (int)(frag / KP), q = (int)(frag - (int64_t)jb * KP);
+  const int n = 32 * jb + (l & 31);
+  const int k = (32 * q + 16 * (l >> 5)) / (int)sizeof(T);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (n < N && k < K) v = *(const u32x4*)(src + (size_t)n * ld + k);
+  *(u32x4*)((char*)dst + (size_t)frag * 1024 + l * 16) = v;
+}
+
+// Blocked copy of an MN-contiguous source (element (n, k) at src[k * ld + n]; N a multiple of 16
+// bytes' worth): block (jb, g) stages the 128 bytes' worth of K rows of K-pairs 4g .. 4g + 3 by 32
+// columns in LDS, then each thread gathers one 16-byte piece down a column. Grid: (NB, ceil(KP / 4)).
+template <typename T>
+__global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src, int64_t ld, int N, int K, int KP,
+                                                       T* __restrict__ dst) {
+  constexpr int kEsz = (int)sizeof(T);
+  constexpr int kVec = 16 / kEsz;            // elements per piece
+  constexpr int kRows = 128 / kEsz;          // K rows of four K-pairs
+  constexpr int kPieces = 32 / kVec;         // pieces per K row of 32 columns
+  static_assert(kRows * kPieces == 256, "one piece per thread");
+  typedef T vec_t __attribute__((ext_vector_type(kVec)));
+  __shared__ __attribute__((aligned(16))) T tile[kRows][32];
+  const int jb = blockIdx.x, grp = blockIdx.y;
+  const int t = threadIdx.x;
+  {
+    const int r = t / kPieces, pc = t % kPieces;
+    const int k = grp * kRows + r, n = 32 * jb + pc * kVec;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (k < K && n < N) v = *(const u32x4*)(src + (size_t)k * ld + n);
+    *(u32x4*)&tile[r][pc * kVec] = v;
+  }
+  __syncthreads();
+  const int q = grp * 4 + (t >> 6);
+  if (q >= KP) return;
+  const int l = t & 63;
+  const int kr = (t >> 6) * (32 / kEsz) + (l >> 5) * kVec;
+  vec_t v;
+#pragma unroll
+  for (int e = 0; e < kVec; ++e) v[e] = tile[kr + e][l & 31];
+  *(vec_t*)((char*)dst + ((size_t)jb * KP + q) * 1024 + l * 16) = v;
+}
+
+// g.B: the blocked copy of B; g.ldb: its KP. Splits must start at whole K-tiles (k_per_split).
+template <typename T, int EPI, bool A_MN, bool KCHECK>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs g) {
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  constexpr int kEsz = (int)sizeof(T);
+  constexpr int kBK = kTileBytes / kEsz;
+  constexpr bool kSwap = (EPI == EPI_STORE || EPI == EPI_DW);
+
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+
+  const int total = g.tiles_m * g.tiles_n * g.splits;
+  int tm, rest;
+  tile_coords(blockIdx.x, total, g.tiles_m, g.group_m, tm, rest);
+  tm = __builtin_amdgcn_readfirstlane(tm);
+  rest = __builtin_amdgcn_readfirstlane(rest);
+  const int tn = rest % g.tiles_n;
+  const int split = rest / g.tiles_n;
+  const int m0 = tm * kTile, n0 = tn * kTile;
+  const int kb = split * g.k_per_split;
+  const int ke = min(g.K, kb + g.k_per_split);
+
+  Operand<T, A_MN> opa;
+  opa.init(g.A, g.lda, m0, min(kTile, g.M - m0), kb, ke, w, lane, wm * 128);
+  const int khalf = lane >> 5;
+  int swi[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) swi[i] = swz_k(i * 32 + (lane & 31));
+
+  // B: this wave's four column blocks start at jb0; K-pair q of this split is fragment q0 + q.
+  const int KP = (int)g.ldb;
+  const int NB = (g.N + 31) >> 5;
+  const __amdgpu_buffer_rsrc_t rb =
+      make_rsrc(g.B, __builtin_amdgcn_readfirstlane((uint32_t)NB * (uint32_t)KP * 1024u));
+  const int jb0 = (n0 + wn * 128) >> 5;
+  const uint32_t bvoff = (uint32_t)lane * 16u;
+  const int q0 = kb * kEsz / 32;
+  const int qend = ((ke - kb) * kEsz + 31) / 32;
+
+  // Quarter pc of A K-tile t (loads 2 pc, 2 pc + 1) into ring slot t % 4.
+  auto load_a_q = [&](int t, auto pc) {
+    constexpr int pq = decltype(pc)::value;
+    const __amdgpu_buffer_rsrc_t r = opa.rsrc(t);
+    char* st = smem + (t & (kXbASlots - 1)) * kOperandBytes + w * 8 * 1024;
+#pragma unroll
+    for (int j = 2 * pq; j < 2 * pq + 2; ++j) {
+      if constexpr (KCHECK && !A_MN) dma16(r, st + j * 1024, opa.offset(t, j));
+      else dma16(r, st + j * 1024, opa.lane_offset(j), opa.uniform_offset(t, j));
+    }
+  };
+  auto load_a = [&](int t) {
+    load_a_q(t, std::integral_constant<int, 0>{});
+    load_a_q(t, std::integral_constant<int, 1>{});
+    load_a_q(t, std::integral_constant<int, 2>{});
+    load_a_q(t, std::integral_constant<int, 3>{});
+  };
+  f32x4 vb[8][4];
+  // B K-pair q into ring slot `slot` (a constant, so that the ring stays in registers).
+  auto load_b = [&](int q, auto slot) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int col = nw + 32 * j + l32;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-          if (row < g.M) mx = fmaxf(mx, acc[i][j][r]);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float ml = mx * kLog2e;
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-          const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
-          s += e;
-          acc[i][j][r] = e * Storage<T>::kE;
-        }
-      s += __shfl_xor(s, 32);
-      if (col < g.N) {
-        if constexpr (EPI == EPI_LSE_BWD) {
-          T* e_row = (T*)g.out + (size_t)col * g.ldo;
-          if constexpr (kEsz == 2) {
-            // Whole 128-row wave slices: e's pitch is M rounded up to 128, and rows at or beyond M
-            // hold exp = 0 here.
-#pragma unroll
-            for (int i = 0; i < 4; ++i) store_row32(e_row + mw + 32 * i, acc[i][j], true, true);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const int row = mw + 32 * i + 8 * q + sub4;
-                if (row < g.M)
-                  store4(e_row + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                         acc[i][j][4 * q + 3]);
-              }
-          }
-        }
-        if (lane < 32) {
-          g.pmax[(size_t)slice * g.ldp + col] = mx;
-          g.psum[(size_t)slice * g.ldp + col] = s;
-        }
-      }
+      const uint32_t so = q < qend ? (uint32_t)((jb0 + j) * KP + q0 + q) * 1024u : kOOB;
+      vb[decltype(slot)::value][j] = __builtin_bit_cast(f32x4, load16(rb, bvoff, __builtin_amdgcn_readfirstlane(so)));
     }
-  } else {
-    // Swapped layout: lane owns rows mw + 32i + l%32 and 4 consecutive columns per (j, q).
-    // N (the output pitch) is a multiple of 4 here, so a 4-column group is all in or all out.
-    const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
+  };
+
+  f32x16 acc[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = mw + 32 * i + l32;
-      if (row >= g.M) continue;
-      if constexpr (EPI == EPI_STORE) {
-        if (g.mode == 1) {
-          float* o = (float*)g.out + (size_t)split * g.M * g.ldo + (size_t)row * g.ldo;
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16){};
+
+  f32x4 fa[2][4];
+  auto read_frags = [&](int t, int p, int buf) {
+    const char* sa = smem + (t & (kXbASlots - 1)) * kOperandBytes;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              if (col < g.N)
-                store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-            }
-        } else {
-          T* o = (T*)g.out + (size_t)row * g.ldo;
-          if constexpr (kEsz == 2) {
-            // N is a multiple of 8 for 16-bit types, so an 8-column piece is all in or all out.
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              if constexpr (Storage<T>::kDzUnscaled) acc[i][j] *= sc;
-              const int c0 = nw + 32 * j + 8 * (lane >> 5);
-              store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
-            }
-          } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const int col = nw + 32 * j + 8 * q + sub4;
-                if (col < g.N)
-                  store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              }
-          }
-        }
-      } else if constexpr (kPreload) {  // EPI_DW, bf16: the accumulators already hold the earlier chunks' sum
-        T* o = (T*)g.out + (size_t)row * g.ldo;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int c0 = nw + 32 * j + 8 * (lane >> 5);
-          store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
-        }
-      } else {  // EPI_DW, fp32 and fp16: add the earlier chunks' sum here
-        T* o = (T*)g.out + (size_t)row * g.ldo;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          f32x4 base[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int col = nw + 32 * j + 8 * q + sub4;
-            base[q] = (!kPreload && accumulate && col < g.N) ? load4(o + col) : (f32x4){};
-          }
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int col = nw + 32 * j + 8 * q + sub4;
-            if (col < g.N)
-              store4(o + col, base[q][0] + sc * acc[i][j][4 * q], base[q][1] + sc * acc[i][j][4 * q + 1],
-                     base[q][2] + sc * acc[i][j][4 * q + 2], base[q][3] + sc * acc[i][j][4 * q + 3]);
-          }
-        }
-      }
+    for (int i = 0; i < 4; ++i) fa[buf][i] = opa.fragment(sa, p, i, khalf, swi[i]);
+  };
+  // See gemm_kernel: transposing reads are invisible to the compiler's waits.
+  auto sync_frags = [&]() {
+    if constexpr (A_MN && kEsz == 2) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(fa[0][0]), "+v"(fa[0][1]), "+v"(fa[0][2]), "+v"(fa[0][3]), "+v"(fa[1][0]),
+                     "+v"(fa[1][1]), "+v"(fa[1][2]), "+v"(fa[1][3])
+                   :
+                   : "memory");
     }
+  };
+  auto mma = [&](int buf, auto slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (kSwap) mfma_pair<T>(acc[i][j], vb[decltype(slot)::value][j], fa[buf][i]);
+        else mfma_pair<T>(acc[i][j], fa[buf][i], vb[decltype(slot)::value][j]);
+      }
+  };
+  constexpr int kReads = A_MN ? 0 : 4;  // compiler-visible LDS reads per section
+  // The section's LDS reads after its first MFMAs, its six loads after MFMAs 1, 3, .., 11.
+  auto sched = []() {
+    if constexpr (kEsz != 2) return;  // fp32: 64 MFMAs per section; left to the compiler
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if ((i & 1) && i < 12) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Section s (0..7) of the K-tile pair starting at kt (even): K-tile kt' = kt + s/4, K-pair
+  // p = s%4, K-pair q = 4 kt + s of the split. The compiler waits for B's registers itself. At
+  // p == 3, A(kt' + 1) has landed in LDS for every wave before K-pair 0 of it is read: its last
+  // quarter went out in section 4 (kt' + 1 - ahead) + 3, and each of the 4 ahead - 5 sections
+  // since issued six loads (loads retire in order).
+  constexpr int kAWait = 6 * (4 * kXbAhead - 5);
+  static_assert(kXbAhead >= 2 && kAWait <= 63, "vmcnt range");
+  auto section = [&](int kt, auto sc) {
+    constexpr int s = decltype(sc)::value;
+    constexpr int p = s & 3;
+    const int ktp = kt + (s >> 2);
+    if constexpr (p == 3) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAWait) : "memory");
+    sync_frags();
+    if constexpr (p == 3) read_frags(ktp + 1, 0, (s + 1) & 1);
+    else read_frags(ktp, p + 1, (s + 1) & 1);
+    load_a_q(ktp + kXbAhead, std::integral_constant<int, p>{});
+    mma(s & 1, std::integral_constant<int, s>{});
+    load_b(4 * kt + s + 7, std::integral_constant<int, (s + 7) & 7>{});
+    sched();
+  };
+
+  const int mw = m0 + wm * 128, nw = n0 + wn * 128;
+  constexpr bool kPreload = EPI == EPI_DW && std::is_same<T, bf16>::value;
+  const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
+  bf16x4 prev[kPreload ? 4 : 1][4][4];
+  if constexpr (kPreload) {
+    if (accumulate) load_dw_prev(g, prev, mw, nw, lane);
   }
+  // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
+  const int nk = (ke - kb + kBK - 1) / kBK;
+  if (nk > 0) {
+    // Prologue: A(0 .. ahead-1), then B(0 .. 6). A(0) has landed for every wave (issued after it:
+    // the other A K-tiles and 28 B loads) before its first fragments are read; the first waits at
+    // p == 3 find at least as many loads after A(1), A(2) as they allow. The dW values (128 VGPRs
+    // raw) become accumulators before B's ring fills the registers.
+#pragma unroll
+    for (int t = 0; t < kXbAhead; ++t) load_a(t);
+    if constexpr (kPreload) {
+      if (accumulate) apply_dw_prev(acc, prev);
+    }
+    load_b(0, std::integral_constant<int, 0>{});
+    load_b(1, std::integral_constant<int, 1>{});
+    load_b(2, std::integral_constant<int, 2>{});
+    load_b(3, std::integral_constant<int, 3>{});
+    load_b(4, std::integral_constant<int, 4>{});
+    load_b(5, std::integral_constant<int, 5>{});
+    load_b(6, std::integral_constant<int, 6>{});
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(8 * (kXbAhead - 1) + 28) : "memory");
+    read_frags(0, 0, 0);
+    for (int kt = 0; kt < nk; kt += 2) {
+      section(kt, std::integral_constant<int, 0>{});
+      section(kt, std::integral_constant<int, 1>{});
+      section(kt, std::integral_constant<int, 2>{});
+      section(kt, std::integral_constant<int, 3>{});
+      section(kt, std::integral_constant<int, 4>{});
+      section(kt, std::integral_constant<int, 5>{});
+      section(kt, std::integral_constant<int, 6>{});
+      section(kt, std::integral_constant<int, 7>{});
+    }
+    // Loads past the end may still be in flight (they target no memory); their LDS and registers
+    // must not be reused before they retire.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+
+  gemm_epilogue<T, EPI, kPreload>(g, acc, mw, nw, split, accumulate);
 }
 
 }  // namespace lce

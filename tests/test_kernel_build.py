@@ -16,11 +16,15 @@ import pytest
 
 from paper_2603_16428_amd import build as B
 
-# (epilogue, A MN-contiguous, B MN-contiguous) of the four GEMMs: logits (forward / backward), dH, dW.
-VARIANTS = [(0, 0, 0), (1, 0, 0), (2, 0, 1), (3, 1, 1)]
 # Element types: bf16 (DF16b), fp16 (DF16_), fp32 (f).
-GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li{e}ELb{a}ELb{b}EEEvNS_8GemmArgsE"
-         for t in ("DF16b", "DF16_", "f") for e, a, b in VARIANTS]
+TYPES = ("DF16b", "DF16_", "f")
+# gemm_kernel (both operands through LDS): the dH GEMM (epilogue 2, A K-contiguous, B MN-contiguous).
+LDS_GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li2ELb0ELb1ELb0EEEvNS_8GemmArgsE" for t in TYPES]
+# gemm_xb_kernel (B from a blocked copy, straight to registers): (epilogue, A MN-contiguous, per-chunk
+# K check) of the logits GEMMs (forward / backward, with and without the K check) and dW.
+XB_VARIANTS = [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1), (3, 1, 0)]
+XB_GEMMS = [f"_ZN3lce14gemm_xb_kernelI{t}Li{e}ELb{a}ELb{c}EEEvNS_8GemmArgsE" for t in TYPES for e, a, c in XB_VARIANTS]
+GEMMS = LDS_GEMMS + XB_GEMMS
 
 
 @pytest.fixture(scope="module")
@@ -65,12 +69,19 @@ def test_gemm_main_loop_has_no_scratch_traffic(asm, name):
     vload = [l for l in loop if l.startswith("buffer_load") and not l.endswith("lds")]
     writes = [l for l in loop if l.startswith("ds_write")]
     tr = [l for l in loop if l.startswith("ds_read_b64_tr_b16")]
-    # Two K-tiles per loop trip: 2 x 64 MFMA steps (x4 for fp32's 32x32x2), 2 x 8 loads of each kind.
+    # Two K-tiles per loop trip: 2 x 64 MFMA steps (x4 for fp32's 32x32x2). gemm_kernel: 2 x 8 loads
+    # of each kind, B written to LDS. gemm_xb_kernel: A by LDS-DMA (2 x 8), B fragments straight to
+    # registers (2 x 16), nothing written to LDS.
     assert len(mfma) == (128 if "DF16" in name else 512), len(mfma)
-    assert len(dma) == 16 and len(vload) == 16 and len(writes) == 16
-    # MN-contiguous 16-bit operands: 2 transposing LDS reads per fragment x 4 fragments per K-pair x
-    # 4 K-pairs per K-tile x 2 K-tiles.
-    n_mn = name.count("ELb1")
+    xb = name in XB_GEMMS
+    if xb:
+        assert len(dma) == 16 and len(vload) == 32 and len(writes) == 0, (len(dma), len(vload), len(writes))
+    else:
+        assert len(dma) == 16 and len(vload) == 16 and len(writes) == 16
+    # MN-contiguous 16-bit operands read from LDS: 2 transposing reads per fragment x 4 fragments per
+    # K-pair x 4 K-pairs per K-tile x 2 K-tiles.
+    flags = [int(f[0]) for f in name.split("ELb")[1:]]
+    n_mn = flags[0] if xb else flags[0] + flags[1]
     assert len(tr) == (2 * 4 * 4 * 2 * n_mn if "DF16" in name else 0), len(tr)
 
 
