@@ -117,25 +117,38 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
   const int nv = *n_valid;
   const float g = Storage<T>::kDzUnscaled ? Storage<T>::kDz : (mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f);
   constexpr float kInvE = 1.f / Storage<T>::kE;
+  constexpr int kPasses = 64 / kRowsPerPass;
   const int tc = threadIdx.x % kTpr, tr = threadIdx.x / kTpr;
   const int v = v0 + tc * kVec;
-  for (int r = tr; r < 64; r += kRowsPerPass) {
-    const int i = i0 + r;
-    const int64_t lab = i < rows ? y[i] : ignore_index;
-    T outv[kVec];
-    if (i < rows && lab != ignore_index) {
-      const float c = g * kInvE * __expf(pmax[(size_t)slice * ldp + i] - lse[i]);
-      T ev[kVec];
-      *(uint4*)ev = *(const uint4*)(ez + (size_t)i * ldz + v);
+  // All of the thread's rows are read, unconditionally, before any is written: stores to the same
+  // buffer, or loads under a branch, would leave one load in flight per thread, and HBM needs
+  // more. Rows at or beyond `rows` (inside the chunk's padded rows, so in bounds) read stale data
+  // that the select below discards; labels and lse are read at a clamped row.
+  uint4 raw[kPasses];
+  float c[kPasses];
+  bool active[kPasses];
 #pragma unroll
-      for (int e = 0; e < kVec; ++e) {
-        float d = (v + e < V) ? c * to_f32(ev[e]) : 0.f;
-        if (v + e == lab) d -= g;
-        outv[e] = from_f32<T>(d);
-      }
-    } else {
+  for (int q = 0; q < kPasses; ++q) {
+    const int i = i0 + tr + q * kRowsPerPass;
+    const int ic = min(i, rows - 1);
+    const int64_t lab = y[ic];
+    const float pm = pmax[(size_t)slice * ldp + i];
+    const float ls = lse[ic];
+    raw[q] = *(const uint4*)(ez + (size_t)i * ldz + v);
+    active[q] = i < rows && lab != ignore_index;
+    c[q] = g * kInvE * __expf(pm - ls);
+  }
 #pragma unroll
-      for (int e = 0; e < kVec; ++e) outv[e] = from_f32<T>(0.f);
+  for (int q = 0; q < kPasses; ++q) {
+    const int i = i0 + tr + q * kRowsPerPass;
+    const int64_t lab = y[min(i, rows - 1)];
+    T ev[kVec], outv[kVec];
+    *(uint4*)ev = raw[q];
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) {
+      float d = (active[q] && v + e < V) ? c[q] * to_f32(ev[e]) : 0.f;
+      if (active[q] && v + e == lab) d -= g;
+      outv[e] = from_f32<T>(d);
     }
     *(uint4*)(ez + (size_t)i * ldz + v) = *(const uint4*)outv;
   }
