@@ -59,7 +59,7 @@ def measured_traffic(workload: str, kind: str):
     if not m:
         return None
     rec = json.loads(m.group(1))
-    if rec.get("source_hash") != kernel_source_hash():
+    if rec.get("source_hash") != kernel_source_hash() or rec.get("workload") != workload:
         return None
     k = rec.get("per_launch", {}).get(kind)
     return None if k is None else int(k["fetch_bytes"] + k["write_bytes"])
@@ -160,6 +160,9 @@ def main():
     log(f"kernel sources {kernel_source_hash()}")
     t0 = time.time()
     d = workloads.make_inputs(args.workload, seed=0, dtype=args.dtype)
+    # The workload as reported (and as its stored counter summaries are named): the dtype is part
+    # of it when it is not the workload's own.
+    wl_name = args.workload if args.dtype is None else f"{args.workload}_{args.dtype}"
     N, H, V = d["N"], d["H"], d["V"]
     log(f"inputs {args.workload} N={N} H={H} V={V} ready in {time.time() - t0:.1f}s")
     dev = torch.device("cuda:0")
@@ -210,7 +213,7 @@ def main():
     per_launch_flops = 2.0 * N * H * V * args.steps / dom_launches
     achieved = per_launch_flops / (dom_ms / dom_launches * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": measured_traffic(args.workload, dom), "kernel": dom,
+                "frac": round(achieved / peak, 4), "traffic": measured_traffic(wl_name, dom), "kernel": dom,
                 "per_launch_flops": per_launch_flops, "avg_launch_ms": dom_ms / dom_launches,
                 "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()}}
 
@@ -297,7 +300,7 @@ def main():
         "scaling": "weak", "vs_baseline": None,
         "dtype": {torch.bfloat16: "bf16", torch.float16: "f16", torch.float32: "f32"}[dtype],
         "data": "synthetic", "tflops": round(tflops, 1), "mfma_peak_frac": round(tflops / peak, 4),
-        "config": {"workload": args.workload if args.dtype is None else f"{args.workload}_{args.dtype}",
+        "config": {"workload": wl_name,
                    "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
         "roofline": roofline, "forward_only": forward_only, "rmsnorm_fused": rmsnorm, "head_train_step": head,

@@ -40,10 +40,12 @@ def asm():
 
 
 def _main_loop(asm_text, name, with_prologue=False):
+    # The K-loop: the innermost loop (gemm_xb_kernel runs it inside a loop over tiles).
     start = asm_text.index(name + ":")
     end = asm_text.index(".Lfunc_end", start)
     body = asm_text[start:end].splitlines()
-    lo = next(i for i, l in enumerate(body) if "Loop Header" in l)
+    depth = max(int(m.group(1)) for l in body for m in [re.search(r"Loop Header: Depth=(\d+)", l)] if m)
+    lo = next(i for i, l in enumerate(body) if f"Loop Header: Depth={depth}" in l)
     hi = next(i for i, l in enumerate(body) if i > lo and "s_cbranch" in l)
     if with_prologue:
         lo = 0
