@@ -8,8 +8,9 @@ peak (credited work 6*N*H*V), the live roofline of the dominant kernel (HIP even
 library on its launch stream), the forward-only rate (loss without gradients, 2*N*H*V), the step
 with the final RMSNorm fused in front (lce_rmsnorm_forward_backward), a training step of the output
 layer with host-resident weights and its hiding factor (lce_head_train_step), peak
-device memory against a materialised-logits PyTorch baseline, and the float64 CPU oracle timed on
-a bounded sample of the same workload.
+device memory against a materialised-logits PyTorch baseline, the median and fastest single step,
+the three contraction shapes of one chunk as plain hipBLASLt GEMMs (context), and the float64 CPU
+oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -141,6 +142,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
     ap.add_argument("--no-rmsnorm", action="store_true", help="skip timing the variant with the final RMSNorm")
+    ap.add_argument("--no-blas", action="store_true", help="skip the hipBLASLt GEMMs timed as context")
     ap.add_argument("--no-head-train", action="store_true",
                     help="skip the output-layer training step with host-resident weights")
     ap.add_argument("--vocab-blocks", type=int, default=8, help="pipeline blocks of the head training step")
@@ -188,14 +190,19 @@ def main():
 
     stream = torch.cuda.current_stream()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     lce.timing_enable(True)
     torch.cuda.synchronize()
     start.record(stream)
-    for _ in range(args.steps):
+    for k in range(args.steps):
         lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
+        if k < args.steps - 1:
+            marks[k].record(stream)
     stop.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
+    bounds = [start] + marks[:args.steps - 1] + [stop]
+    per_step = sorted(bounds[k].elapsed_time(bounds[k + 1]) for k in range(args.steps))
     kern = lce.timing_read()
     lce.timing_enable(False)
     ms = total_ms / args.steps
@@ -216,6 +223,33 @@ def main():
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(wl_name, dom), "kernel": dom,
                 "per_launch_flops": per_launch_flops, "avg_launch_ms": dom_ms / dom_launches,
                 "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()}}
+
+    # Context: the three contraction shapes of one chunk as plain hipBLASLt GEMMs (torch.mm, 2-D
+    # operands; no epilogue work, no log-sum-exp, no dlogits).
+    blas = None
+    if not args.no_blas and dtype != torch.float32:
+        nc = chunk
+        Xc = X[:nc]
+        dZ = (torch.randn(nc, V, device=dev) * 1e-4).to(dtype)
+        shapes = {"logits": (Xc, W.t()), "dh": (dZ, W), "dw": (dZ.t(), Xc)}
+        blas = {}
+        for name, (a, b) in shapes.items():
+            for _ in range(3):
+                c = a @ b
+            torch.cuda.synchronize()
+            b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            b0.record(stream)
+            for _ in range(10):
+                c = a @ b
+            b1.record(stream)
+            torch.cuda.synchronize()
+            bms = b0.elapsed_time(b1) / 10
+            blas[f"{name}_ms"] = round(bms, 4)
+            blas[f"{name}_tflops"] = round(2.0 * nc * H * V / (bms * 1e-3) / 1e12, 1)
+            del c
+        del dZ, shapes
+        torch.cuda.empty_cache()
+        log("hipBLASLt context (one chunk's shapes): " + ", ".join(f"{k} {v}" for k, v in blas.items()))
 
     # Forward only (loss, no gradients): 2 N H V credited flops per call, reported beside the step.
     fws = torch.empty(lce.workspace_size(N, H, V, dtype, False), dtype=torch.uint8, device=dev)
@@ -296,7 +330,9 @@ def main():
 
     result = {
         "metric": METRIC, "value": round(N / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(per_step[len(per_step) // 2], 4), "ms_per_step_min": round(per_step[0], 4),
+        "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": {torch.bfloat16: "bf16", torch.float16: "f16", torch.float32: "f32"}[dtype],
         "data": "synthetic", "tflops": round(tflops, 1), "mfma_peak_frac": round(tflops / peak, 4),
@@ -304,7 +340,7 @@ def main():
                    "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
         "roofline": roofline, "forward_only": forward_only, "rmsnorm_fused": rmsnorm, "head_train_step": head,
-        "memory": memory,
+        "memory": memory, "hipblaslt_context": blas,
     }
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host cores ...")
