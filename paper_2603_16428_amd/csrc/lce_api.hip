@@ -291,7 +291,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
 
     {
     KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)cdiv(rows, 32)), dim3(256), 0, s, pmax, psum, p.ncp,
+    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)cdiv(rows, kCombineTokens)), dim3(256), 0, s, pmax, psum, p.ncp,
                        (int)p.slices, rows, y + t0, ignore_index, tgt + t0, lse + t0, tl + t0);
     }
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;

@@ -63,34 +63,36 @@ __global__ __launch_bounds__(256) void target_logit_kernel(const T* __restrict__
 }
 
 // Row combine. For each token of the chunk: M = max_t m_t, lse = M + log sum_t s_t exp(m_t - M),
-// and the token loss lse - z_target (0 for ignored tokens). 32 tokens x 8 slice-groups per block;
-// each thread merges its slices in increasing order, then the 8 groups merge in a fixed order.
+// and the token loss lse - z_target (0 for ignored tokens). A block takes 16 tokens x 16 slice
+// groups: thread (token j, group k) merges slices k, k + 16, ... in increasing order (a 64-byte
+// coalesced row of partials per slice), then group 0 merges the 16 groups in a fixed order.
+constexpr int kCombineTokens = 16;
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ pmax, const float* __restrict__ psum,
                                                       int64_t ldp, int slices, int rows,
                                                       const int64_t* __restrict__ y, int64_t ignore_index,
                                                       const float* __restrict__ tgt,
                                                       float* __restrict__ lse_out,     // [rows] (chunk-offset)
                                                       float* __restrict__ loss_out) {  // [rows] (chunk-offset)
-  __shared__ float sm[8][32], ss[8][32];
-  const int t = threadIdx.x & 31, gidx = threadIdx.x >> 5;
-  const int i = blockIdx.x * 32 + t;
+  __shared__ float sm[16][kCombineTokens], ss[16][kCombineTokens];
+  const int t = threadIdx.x % kCombineTokens, grp = threadIdx.x / kCombineTokens;
+  const int i = blockIdx.x * kCombineTokens + t;
   float m = -INFINITY, s = 0.f;
   if (i < rows) {
-    for (int k = gidx; k < slices; k += 8) {
+    for (int k = grp; k < slices; k += 16) {
       const float mk = pmax[(size_t)k * ldp + i], sk = psum[(size_t)k * ldp + i];
       const float mn = fmaxf(m, mk);
       s = s * __expf(m - mn) + sk * __expf(mk - mn);
       m = mn;
     }
   }
-  sm[gidx][t] = m;
-  ss[gidx][t] = s;
+  sm[grp][t] = m;
+  ss[grp][t] = s;
   __syncthreads();
-  if (gidx == 0 && i < rows) {
+  if (grp == 0 && i < rows) {
     float M = sm[0][t];
-    for (int k = 1; k < 8; ++k) M = fmaxf(M, sm[k][t]);
+    for (int k = 1; k < 16; ++k) M = fmaxf(M, sm[k][t]);
     float S = 0.f;
-    for (int k = 0; k < 8; ++k) S += ss[k][t] * __expf(sm[k][t] - M);
+    for (int k = 0; k < 16; ++k) S += ss[k][t] * __expf(sm[k][t] - M);
     const float lse = M + __logf(S);
     lse_out[i] = lse;
     loss_out[i] = (y[i] == ignore_index) ? 0.f : lse - tgt[i];
