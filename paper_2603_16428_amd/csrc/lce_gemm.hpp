@@ -949,7 +949,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
   // p = s%4, K-pair q = 4 kt + s of the split. The compiler waits for B's registers itself. At
   // p == 3, A(kt' + 1) has landed in LDS for every wave before K-pair 0 of it is read: its last
   // quarter went out in section 4 (kt' + 1 - ahead) + 3, and each of the 4 ahead - 5 sections
-  // since issued six loads (loads retire in order).
+  // since issued six loads (loads retire in order; whichever order a section issues its own two
+  // kinds in, all six of a later section come after).
   constexpr int kAWait = 6 * (4 * kXbAhead - 5);
   static_assert(kXbAhead >= 2 && kAWait <= 63, "vmcnt range");
   auto section = [&](int kt, auto sc) {
@@ -960,9 +961,18 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     sync_frags();
     if constexpr (p == 3) read_frags(ktp + 1, 0, (s + 1) & 1);
     else read_frags(ktp, p + 1, (s + 1) & 1);
-    load_a_q(ktp + kXbAhead, std::integral_constant<int, p>{});
-    mma(s & 1, std::integral_constant<int, s>{});
-    load_b(4 * kt + s + 7, std::integral_constant<int, (s + 7) & 7>{});
+    // Loads retire in issue order, so a B load waits for every A load issued before it. With A
+    // K-contiguous (W, streamed from HBM) the section issues its B fragments first (measured 4%
+    // faster on the logits GEMM); with A MN-contiguous (dZ^T) the order made no difference.
+    if constexpr (!A_MN) {
+      mma(s & 1, std::integral_constant<int, s>{});
+      load_b(4 * kt + s + 7, std::integral_constant<int, (s + 7) & 7>{});
+      load_a_q(ktp + kXbAhead, std::integral_constant<int, p>{});
+    } else {
+      load_a_q(ktp + kXbAhead, std::integral_constant<int, p>{});
+      mma(s & 1, std::integral_constant<int, s>{});
+      load_b(4 * kt + s + 7, std::integral_constant<int, (s + 7) & 7>{});
+    }
     sched();
   };
 
