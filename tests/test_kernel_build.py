@@ -161,3 +161,92 @@ def test_mn_contiguous_bf16_layout_model():
                             banks = [((a // 4) + b) % nb for a in addrs[g0:g0 + grp] for b in (0, 1)]
                             conflicts += len(banks) - len(set(banks))
     assert conflicts == 0
+
+
+# ---- Blocked operand B of gemm_xb_kernel: the two blocking kernels and the GEMM's loads ---------
+# Restated from block_k_kernel, block_mn_kernel and gemm_xb_kernel's load_b: both blocking kernels
+# must put element (n, k) at the same byte, and the GEMM's B load for K-pair q of column block jb
+# must hand lane l the column and the K bytes that the A fragment of the same lane covers (K-pair
+# q = 4 t + p of K-tile t, lane half h: bytes [32 q + 16 h, +16) of the row).
+
+def _blocked_from_k(N, K, esz, KP, NB):
+    out = {}  # byte -> (n, k) of the element there, or None for padding
+    for frag in range(NB * KP):
+        jb, q = divmod(frag, KP)
+        for l in range(64):
+            n, k = 32 * jb + (l & 31), (32 * q + 16 * (l >> 5)) // esz
+            for e in range(16 // esz):
+                out[frag * 1024 + l * 16 + e * esz] = (n, k + e) if (n < N and k < K) else None
+    return out
+
+
+def _blocked_from_mn(N, K, esz, KP, NB):
+    vec, rows, pieces = 16 // esz, 128 // esz, 32 // (16 // esz)
+    out = {}
+    for jb in range(NB):
+        for grp in range((KP + 3) // 4):
+            tile = {}
+            for t in range(256):   # staging: thread t loads row t / pieces, piece t % pieces
+                r, pc = divmod(t, pieces)
+                k, n = grp * rows + r, 32 * jb + pc * vec
+                for e in range(vec):
+                    tile[(r, pc * vec + e)] = (n + e, k) if (k < K and n < N) else None
+            for t in range(256):   # gather: thread t writes lane t % 64 of fragment 4 grp + t / 64
+                q = grp * 4 + (t >> 6)
+                if q >= KP:
+                    continue
+                l = t & 63
+                kr = (t >> 6) * (32 // esz) + (l >> 5) * vec
+                for e in range(vec):
+                    out[(jb * KP + q) * 1024 + l * 16 + e * esz] = tile[(kr + e, l & 31)]
+    return out
+
+
+def _check_definition(layout, N, K, esz, KP, NB):
+    # Every element of B appears once, at the byte the layout defines; everything else is padding.
+    placed = [v for v in layout.values() if v is not None]
+    assert sorted(placed) == sorted((n, k) for n in range(N) for k in range(K))
+    for byte, v in layout.items():
+        if v is not None:
+            frag, rem = divmod(byte, 1024)
+            l, off = divmod(rem, 16)
+            jb, q = divmod(frag, KP)
+            assert v == (32 * jb + (l & 31), (32 * q + 16 * (l >> 5) + off) // esz)
+
+
+@pytest.mark.parametrize("N,K,esz", [(70, 200, 2), (33, 40, 4)])
+def test_blocked_from_k_ragged_columns(N, K, esz):
+    # block_k_kernel (logits GEMM: columns = tokens, any count; K = H, whole 16-byte pieces).
+    KP = -(-(K * esz) // 128) * 128 // 32
+    NB = -(-N // 32)
+    _check_definition(_blocked_from_k(N, K, esz, KP, NB), N, K, esz, KP, NB)
+
+
+@pytest.mark.parametrize("N,K,esz", [(72, 37, 2), (36, 13, 4)])
+def test_blocked_from_mn_ragged_k(N, K, esz):
+    # block_mn_kernel (dW GEMM: columns = H, whole 16-byte pieces; K = tokens, any count).
+    KP = -(-(K * esz) // 128) * 128 // 32
+    NB = -(-N // 32)
+    _check_definition(_blocked_from_mn(N, K, esz, KP, NB), N, K, esz, KP, NB)
+
+
+# N and K as both kernels require (whole 16-byte pieces on both axes), so that both apply.
+@pytest.mark.parametrize("N,K,esz", [(72, 200, 2), (64, 256, 2), (36, 40, 4), (96, 72, 4), (8, 8, 2)])
+def test_blocked_operand_layout_model(N, K, esz):
+    KP = -(-(K * esz) // 128) * 128 // 32
+    NB = -(-N // 32)
+    a = _blocked_from_k(N, K, esz, KP, NB)
+    b = _blocked_from_mn(N, K, esz, KP, NB)
+    assert a == b
+    _check_definition(a, N, K, esz, KP, NB)
+    # The GEMM's B loads (wave column blocks jb0 .. jb0 + 3, split starting at K-pair q0 = 0).
+    for jb in range(NB):
+        for q in range(KP):
+            soff = (jb * KP + q) * 1024
+            for l in range(64):
+                got = [a[soff + l * 16 + e * esz] for e in range(16 // esz)]
+                t, p = divmod(q, 4)
+                h = l >> 5
+                kbytes = 128 * t + 32 * p + 16 * h          # the A fragment's K bytes for this lane
+                want = [(32 * jb + (l & 31), kbytes // esz + e) for e in range(16 // esz)]
+                assert [g for g in got if g is not None] == [w for w in want if w[0] < N and w[1] < K]
