@@ -7,10 +7,13 @@
 //   logits^T = W . X_c^T     A = W [V, H] K-contig,        B = X_c [n_c, H] K-contig
 //   dH_c     = dZ_c . W      A = dZ_c [n_c, V] K-contig,   B = W [V, H] MN-contig
 //   dW      += dZ_c^T . X_c  A = dZ_c [n_c, V] MN-contig,  B = X_c [n_c, H] MN-contig
-// so no operand is ever transposed in memory.
+// so W and dZ are never transposed in memory. Two main loops share the tile, waves, fragment
+// reads and epilogues: gemm_kernel (below) takes both operands through LDS and runs dH;
+// gemm_xb_kernel (at the end of this file) reads B from a fragment-blocked copy straight into
+// registers and runs the logits and dW contractions, whose B is the small X chunk.
 //
-// One workgroup computes a 256 x 256 tile of C with four waves (2 x 2), each wave a 128 x 128
-// sub-tile held as 4 x 4 blocks of the 32x32 MFMA accumulator (256 fp32 per lane, in AGPRs). K
+// gemm_kernel. One workgroup computes a 256 x 256 tile of C with four waves (2 x 2), each wave a
+// 128 x 128 sub-tile held as 4 x 4 blocks of the 32x32 MFMA accumulator (256 fp32 per lane). K
 // advances in K-tiles of 64 bf16 (32 fp32); an operand's K-tile is 32 KB of LDS either way:
 // 256 rows of 128 bytes (K-contig) or 64 (32) K-rows of 512 (1024) bytes (MN-contig). Global loads
 // are 16 bytes per lane and read whole 128-byte lines.
