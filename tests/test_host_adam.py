@@ -19,12 +19,18 @@ def lce():
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
 @pytest.mark.parametrize("threads", [1, 3, 0])
-def test_matches_oracle_over_steps(lce, dtype, threads):
+@pytest.mark.parametrize("moment_offset", [0, 1])
+def test_matches_oracle_over_steps(lce, dtype, threads, moment_offset):
+    # moment_offset 0: every array 64-byte aligned (torch's host allocations), so bf16 takes the
+    # streaming AVX-512 body where the host has it; 1: the moments start 4 bytes in, which keeps
+    # every range on the generic body.
     n = 70001 if threads != 1 else 1003          # above the threading cut-off when threaded
     rng = np.random.default_rng(7)
-    p = torch.from_numpy(rng.standard_normal(n).astype(np.float32))
-    m = torch.zeros(n)
-    v = torch.zeros(n)
+    p = torch.empty(n)
+    p.copy_(torch.from_numpy(rng.standard_normal(n).astype(np.float32)))
+    m = torch.zeros(n + moment_offset)[moment_offset:]
+    v = torch.zeros(n + moment_offset)[moment_offset:]
+    assert p.data_ptr() % 64 == 0 and (m.data_ptr() % 64 == 0) == (moment_offset == 0)
     pr, mr, vr = p.double().numpy(), np.zeros(n), np.zeros(n)
     cfg = dict(lr=2e-3, betas=(0.9, 0.95), eps=1e-8, weight_decay=0.05)
     p16 = torch.empty(n, dtype=DT[dtype]) if dtype != "fp32" else None
@@ -73,3 +79,20 @@ def test_bf16_rounding_of_ties_and_nan(lce):
     out = torch.empty(4, dtype=torch.bfloat16)
     lce.host_adam_step(p, g, torch.zeros(4), torch.zeros(4), 1, lr=0.0, param16=out, threads=1)
     assert out[0].item() == 1.0 and out[1].item() == 1.0 + 2 ** -6 and torch.isnan(out[2]) and out[3].item() == -2.5
+
+
+def test_bf16_rounding_in_the_vector_body(lce):
+    # 64 aligned parameters (the streaming AVX-512 body where the host has it): ties round to the
+    # even neighbour, NaN stays NaN, and everything equals torch's own rounding of the fp32 result.
+    vals = [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, float("nan"), -2.5, 3.0e38, -1.0e-40, 0.0, -0.0]
+    p = torch.empty(64)
+    p.copy_(torch.tensor(vals * 8, dtype=torch.float32))
+    g = torch.zeros(64, dtype=torch.bfloat16)
+    out = torch.empty(64, dtype=torch.bfloat16)
+    assert p.data_ptr() % 64 == 0 and out.data_ptr() % 64 == 0
+    lce.host_adam_step(p, g, torch.zeros(64), torch.zeros(64), 1, lr=0.0, param16=out, threads=1)
+    ref = p.to(torch.bfloat16)
+    nan = torch.isnan(p)
+    assert torch.equal(torch.isnan(out), nan)
+    assert torch.equal(out[~nan].view(torch.int16), ref[~nan].view(torch.int16))
+    assert out[0].item() == 1.0 and out[1].item() == 1.0 + 2 ** -6
