@@ -46,7 +46,9 @@ def _main_loop(asm_text, name, with_prologue=False):
     body = asm_text[start:end].splitlines()
     depth = max(int(m.group(1)) for l in body for m in [re.search(r"Loop Header: Depth=(\d+)", l)] if m)
     lo = next(i for i, l in enumerate(body) if f"Loop Header: Depth={depth}" in l)
-    hi = next(i for i, l in enumerate(body) if i > lo and "s_cbranch" in l)
+    # The loop's back edge: the branch to the header's label (the body may hold other branches).
+    label = next(body[i].split(":")[0].strip() for i in range(lo, -1, -1) if re.match(r"^\.LBB\w+:", body[i]))
+    hi = next(i for i, l in enumerate(body) if i > lo and re.match(r"\s*s_(c)?branch\S*\s+" + re.escape(label) + r"\s*$", l))
     if with_prologue:
         lo = 0
     return [l.strip() for l in body[lo:hi + 1] if l.strip() and not l.strip().startswith(";")]
