@@ -992,15 +992,16 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     // Prologue: A(0 .. ahead-1), then B(0 .. 6). A(0) has landed for every wave (issued after it:
     // the other A K-tiles and 28 B loads) before its first fragments are read; the first waits at
     // p == 3 find at least as many loads after A(1), A(2) as they allow. The dW values (128 VGPRs
-    // raw) become accumulators before B's ring fills the registers.
+    // raw) become accumulators once the first three K-pairs of B are on their way, before the rest
+    // of B's ring fills the registers.
 #pragma unroll
     for (int t = 0; t < kXbAhead; ++t) load_a(t);
-    if constexpr (kPreload) {
-      if (accumulate) apply_dw_prev(acc, prev);
-    }
     load_b(0, std::integral_constant<int, 0>{});
     load_b(1, std::integral_constant<int, 1>{});
     load_b(2, std::integral_constant<int, 2>{});
+    if constexpr (kPreload) {
+      if (accumulate) apply_dw_prev(acc, prev);
+    }
     load_b(3, std::integral_constant<int, 3>{});
     load_b(4, std::integral_constant<int, 4>{});
     load_b(5, std::integral_constant<int, 5>{});
