@@ -411,25 +411,34 @@ struct Operand {
   }
 };
 
-// bf16 dW accumulation (chunks after the first): the wave's current dW values in the swapped
+// 16-bit dW accumulation (chunks after the first): the wave's current dW values in the swapped
 // accumulator layout, loaded raw while the pipeline fills, then the accumulators' starting values.
-__device__ __forceinline__ void load_dw_prev(const GemmArgs& g, bf16x4 (&prev)[4][4][4], int mw, int nw, int lane) {
+// They enter divided by the factor the epilogue will apply (the dz storage scale, 1 for bf16), so
+// that the epilogue's one multiply gives dW + factor * (this chunk's sum); a zero factor (a mean
+// over no valid token) starts them at zero.
+template <typename T>
+using vec4_t = T __attribute__((ext_vector_type(4)));
+
+template <typename T>
+__device__ __forceinline__ void load_dw_prev(const GemmArgs& g, vec4_t<T> (&prev)[4][4][4], int mw, int nw, int lane) {
+  typedef vec4_t<T> t4;
   const int sub4 = 4 * (lane >> 5);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = mw + 32 * i + (lane & 31);
-    const bf16* o = (const bf16*)g.out + (size_t)row * g.ldo;
+    const T* o = (const T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int col = nw + 32 * j + 8 * q + sub4;
-        prev[i][j][q] = (row < g.M && col < g.N) ? *(const bf16x4*)(o + col) : (bf16x4){};
+        prev[i][j][q] = (row < g.M && col < g.N) ? *(const t4*)(o + col) : (t4){};
       }
   }
 }
 
-__device__ __forceinline__ void apply_dw_prev(f32x16 (&acc)[4][4], const bf16x4 (&prev)[4][4][4]) {
+template <typename T>
+__device__ __forceinline__ void apply_dw_prev(f32x16 (&acc)[4][4], const vec4_t<T> (&prev)[4][4][4], float inv_scale) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -437,7 +446,21 @@ __device__ __forceinline__ void apply_dw_prev(f32x16 (&acc)[4][4], const bf16x4 
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] = (float)prev[i][j][q][e];
+        for (int e = 0; e < 4; ++e) {
+          const float x = (float)prev[i][j][q][e];
+          acc[i][j][4 * q + e] = Storage<T>::kDzUnscaled ? x * inv_scale : x;
+        }
+}
+
+// The epilogue factor's reciprocal for apply_dw_prev (0 when the factor is 0).
+template <typename T>
+__device__ __forceinline__ float dw_prev_scale(const GemmArgs& g) {
+  if constexpr (!Storage<T>::kDzUnscaled) {
+    return 1.f;
+  } else {
+    const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
+    return sc > 0.f ? 1.f / sc : 0.f;
+  }
 }
 
 // The epilogue: what a wave's 128 x 128 accumulator sub-tile at (mw, nw) becomes. Without the
@@ -544,14 +567,15 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
               }
           }
         }
-      } else if constexpr (PRELOADED) {  // EPI_DW, bf16: the accumulators already hold the earlier chunks' sum
+      } else if constexpr (PRELOADED) {  // EPI_DW, 16-bit: the accumulators already hold the earlier chunks' sum
         T* o = (T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
+          if constexpr (Storage<T>::kDzUnscaled) acc[i][j] *= sc;
           const int c0 = nw + 32 * j + 8 * (lane >> 5);
           store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
         }
-      } else {  // EPI_DW, fp32 and fp16: add the earlier chunks' sum here
+      } else {  // EPI_DW, fp32: add the earlier chunks' sum here
         T* o = (T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -728,16 +752,16 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     mma(1);
     sched(0, 0);
   };
-  // bf16 dW accumulation (chunks after the first): the tile's current dW values are loaded here,
+  // 16-bit dW accumulation (chunks after the first): the tile's current dW values are loaded here,
   // raw, in flight together with the loads that fill the pipeline, and become the accumulators'
   // starting values, so the epilogue only stores. (fp32 adds them in the epilogue instead: its
   // 256 values per lane would not fit next to the pipeline's registers.)
   const int mw = m0 + wm * 128, nw = n0 + wn * 128;
-  constexpr bool kPreload = EPI == EPI_DW && std::is_same<T, bf16>::value;
+  constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
   const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
-  bf16x4 prev[kPreload ? 4 : 1][4][4];
+  vec4_t<T> prev[kPreload ? 4 : 1][4][4];
   if constexpr (kPreload) {
-    if (accumulate) load_dw_prev(g, prev, mw, nw, lane);
+    if (accumulate) load_dw_prev<T>(g, prev, mw, nw, lane);
   }
   // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
   const int nk = (ke - kb + kBK - 1) / kBK;
@@ -747,7 +771,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g)
     load_b(1, P1{});
     load_a(1);
     if constexpr (kPreload) {
-      if (accumulate) apply_dw_prev(acc, prev);
+      if (accumulate) apply_dw_prev<T>(acc, prev, dw_prev_scale<T>(g));
     }
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsPerOperand) : "memory");  // B(0) landed
     write_b(P0{});
@@ -980,11 +1004,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
   };
 
   const int mw = m0 + wm * 128, nw = n0 + wn * 128;
-  constexpr bool kPreload = EPI == EPI_DW && std::is_same<T, bf16>::value;
+  constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
   const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
-  bf16x4 prev[kPreload ? 4 : 1][4][4];
+  vec4_t<T> prev[kPreload ? 4 : 1][4][4];
   if constexpr (kPreload) {
-    if (accumulate) load_dw_prev(g, prev, mw, nw, lane);
+    if (accumulate) load_dw_prev<T>(g, prev, mw, nw, lane);
   }
   // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
   const int nk = (ke - kb + kBK - 1) / kBK;
@@ -1000,7 +1024,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     load_b(1, std::integral_constant<int, 1>{});
     load_b(2, std::integral_constant<int, 2>{});
     if constexpr (kPreload) {
-      if (accumulate) apply_dw_prev(acc, prev);
+      if (accumulate) apply_dw_prev<T>(acc, prev, dw_prev_scale<T>(g));
     }
     load_b(3, std::integral_constant<int, 3>{});
     load_b(4, std::integral_constant<int, 4>{});
