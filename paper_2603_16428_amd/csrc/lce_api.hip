@@ -5,10 +5,11 @@
 //   count valid labels (global mean divisor) -> target logits
 //   for each chunk of n_c tokens:
 //     fragment-blocked copies of X_c (operand B of the logits and dW GEMMs)
-//     logits^T tile GEMM with the log-sum-exp epilogue  (stores e = exp(z - m_slice) for backward)
+//     logits^T tile GEMM with the log-sum-exp epilogue  (stores e = exp(z - m_slice) for backward,
+//                                                       fragment-blocked)
 //     row combine -> lse, token losses
-//     [backward] dlogits in place -> dH rows GEMM (reads W as it is) -> dW GEMM (reads dZ as it
-//                is; the first chunk writes dW, later chunks add to it)
+//     [backward] dlogits in place -> dH rows GEMM (dH^T = W^T dZ^T: reads W as it is) -> dW GEMM
+//                (reads the blocked dZ as it is; the first chunk writes dW, later chunks add to it)
 //   loss reduction (fp64, fixed order)
 #include <hip/hip_runtime.h>
 
@@ -76,13 +77,16 @@ struct Plan {
   int esz = 0;
   bool backward = false;
   int64_t nc = 0, chunks = 0;     // tokens per chunk, number of chunks
-  int64_t Vp = 0, ncp = 0;
+  int64_t ncp = 0;                // tokens per chunk rounded up to 64
   int64_t slices = 0;
   int dh_splits = 1;
   int64_t dh_kps = 0;             // K (vocabulary) per dH split, multiple of the K-tile
   // Fragment-blocked copies of a chunk's X: operand B of the logits GEMM (columns = tokens,
   // K = H) and of the dW GEMM (columns = H, K = tokens): column blocks and K-pairs per block.
   int64_t xk_nb = 0, xk_kp = 0, xm_nb = 0, xm_kp = 0;
+  // e / dZ of a chunk, blocked (columns = tokens, K = vocabulary rounded up to the tile): operand
+  // B of the dH GEMM and blocked operand A of the dW GEMM.
+  int64_t ez_nb = 0, ez_kp = 0;
   // workspace offsets (bytes)
   size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_dhp = 0;
   size_t o_xk = 0, o_xm = 0;
@@ -128,26 +132,28 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   else if (nc % 64 != 0) return LCE_ERR_INVALID_ARGUMENT;
   p.nc = nc;
   p.chunks = cdiv(N, nc);
-  p.Vp = round_up(V, 128);
   p.ncp = round_up(nc, 64);
   p.slices = cdiv(V, kLseSlice);
-  // 32-bit limits: buffer ranges of one 256-row operand slice, and int tile/element indices.
+  // 32-bit limits: buffer ranges of one 256-row operand slice (and of four column blocks of a
+  // blocked operand), and int tile/element indices.
   const int64_t lim = (int64_t(1) << 31) - 1;
-  const int64_t maxpitch = std::max({H, p.Vp});
+  const int64_t maxpitch = std::max({H, round_up(V, kTile)});
   if ((int64_t)kTile * maxpitch * p.esz > lim || N > lim / 2 || V > lim / 2 || H > lim / 2) return LCE_ERR_UNSUPPORTED;
-  if (cdiv(V, kTile) * cdiv(H, kTile) > lim / 16 || cdiv(p.ncp * p.Vp, 2048) > lim) return LCE_ERR_UNSUPPORTED;
+  if (cdiv(V, kTile) * cdiv(H, kTile) > lim / 16) return LCE_ERR_UNSUPPORTED;
   p.xk_nb = cdiv(p.ncp, 32);
   p.xk_kp = round_up(H * p.esz, kTileBytes) / 32;
   p.xm_nb = cdiv(H, 32);
   p.xm_kp = round_up(p.ncp * p.esz, kTileBytes) / 32;
   if (p.xk_nb * p.xk_kp * 1024 > lim || p.xm_nb * p.xm_kp * 1024 > lim) return LCE_ERR_UNSUPPORTED;
+  p.ez_nb = p.ncp / 32;
+  p.ez_kp = round_up(V, kTile) * p.esz / 32;
 
   if (backward) {
     // dH tiles of one chunk: split the vocabulary (K) so that the grid fills the device.
     const int64_t tiles = cdiv(nc, kTile) * cdiv(H, kTile);
     const int cus = query_device ? num_cus() : 256;
     const int64_t kbk = kTileBytes / p.esz;
-    const int64_t kblocks = cdiv(p.Vp, kbk);
+    const int64_t kblocks = cdiv(V, kbk);
     double best = 1e30;
     int best_s = 1;
     for (int s = 1; s <= 8; ++s) {
@@ -175,21 +181,18 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.o_xk = take((size_t)(p.xk_nb * p.xk_kp * 1024));
   if (backward) {
     p.o_xm = take((size_t)(p.xm_nb * p.xm_kp * 1024));
-    p.o_e = take((size_t)p.ncp * p.Vp * p.esz);
+    p.o_e = take((size_t)(p.ez_nb * p.ez_kp * 1024));
     if (p.dh_splits > 1 || dx_f32) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
   }
   p.total = off;
   return LCE_OK;
 }
 
-// KCHECK: a K-contig operand's K range may end inside a K-tile and its rows are not zero-padded
-// up to the next one (see Operand::offset). XB: operand B is a fragment-blocked copy, read by
-// gemm_xb_kernel (B_MN is then ignored).
-template <typename T, int EPI, bool A_MN, bool B_MN, bool KCHECK = false, bool XB = false>
+// AL: operand A's layout (ALayout); operand B is blocked. KCHECK: a K-contig A's K range may end
+// inside a K-tile and its rows are not zero-padded up to the next one (see Operand::offset).
+template <typename T, int EPI, int AL, bool KCHECK = false>
 hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
-  const void* fn = XB ? (const void*)gemm_xb_kernel<T, EPI, A_MN, KCHECK>
-                      : (const void*)gemm_kernel<T, EPI, A_MN, B_MN, KCHECK>;
-  const int smem = XB ? kXbSmem : kGemmSmem;
+  const void* fn = (const void*)gemm_xb_kernel<T, EPI, AL, KCHECK>;
   static std::atomic<uint64_t> configured[kMaxDevices / 64 + 1];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -197,7 +200,7 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   if (dev < kMaxDevices) {
     const uint64_t bit = uint64_t(1) << (dev & 63);
     if (!(configured[dev >> 6].load() & bit)) {
-      e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+      e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kXbSmem);
       if (e != hipSuccess) return e;
       configured[dev >> 6].fetch_or(bit);
     }
@@ -206,11 +209,7 @@ hipError_t launch_gemm(GemmArgs g, hipStream_t s) {
   g.tiles_n = (int)cdiv(g.N, kTile);
   const int blocks = g.tiles_m * g.tiles_n * g.splits;
   if (blocks <= 0) return hipSuccess;
-  if constexpr (XB) {
-    hipLaunchKernelGGL((gemm_xb_kernel<T, EPI, A_MN, KCHECK>), dim3(blocks), dim3(kGemmThreads), smem, s, g);
-  } else {
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, A_MN, B_MN, KCHECK>), dim3(blocks), dim3(kGemmThreads), smem, s, g);
-  }
+  hipLaunchKernelGGL((gemm_xb_kernel<T, EPI, AL, KCHECK>), dim3(blocks), dim3(kGemmThreads), kXbSmem, s, g);
   return hipGetLastError();
 }
 
@@ -279,12 +278,10 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     // W's rows end at H: whole K-tiles read them unchecked only when H is made of whole K-tiles.
     const bool whole = H % (kTileBytes / p.esz) == 0;
     if (p.backward) {
-      g.out = ez; g.ldo = p.Vp;
-      e = whole ? launch_gemm<T, EPI_LSE_BWD, false, false, false, true>(g, s)
-                : launch_gemm<T, EPI_LSE_BWD, false, false, true, true>(g, s);
+      g.out = ez; g.ldo = p.ez_kp;
+      e = whole ? launch_gemm<T, EPI_LSE_BWD, A_K, false>(g, s) : launch_gemm<T, EPI_LSE_BWD, A_K, true>(g, s);
     } else {
-      e = whole ? launch_gemm<T, EPI_LSE_FWD, false, false, false, true>(g, s)
-                : launch_gemm<T, EPI_LSE_FWD, false, false, true, true>(g, s);
+      e = whole ? launch_gemm<T, EPI_LSE_FWD, A_K, false>(g, s) : launch_gemm<T, EPI_LSE_FWD, A_K, true>(g, s);
     }
     }
     if (e != hipSuccess) return LCE_ERR_HIP;
@@ -297,19 +294,19 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
     if (!p.backward) continue;
 
-    // dlogits, in place.
+    // dlogits, in place (blocked).
     {
     KernelTimer t(T_DLOGITS, s);
-    hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)(p.Vp / 128), (unsigned)(p.ncp / 64)), dim3(256), 0, s,
-                       ez, p.Vp, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V);
+    hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)(p.ez_kp / 16), (unsigned)p.ez_nb), dim3(256), 0, s,
+                       ez, p.ez_kp, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V);
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
     }
 
-    // dH rows of the chunk = dZ_c . W  (A = dZ_c [rows, Vp] K-contig, B = W [V, H] MN-contig). dZ's
-    // rows are zero-padded to Vp, a multiple of every K-tile, so its loads read whole K-tiles.
+    // dH rows of the chunk, as dH_c^T = W^T . dZ_c^T (A = W [V, H] MN-contig over H, B = dZ_c
+    // blocked over the chunk's tokens), stored token-major.
     GemmArgs gh{};
-    gh.A = ez; gh.lda = p.Vp; gh.M = rows;
-    gh.B = W; gh.ldb = H; gh.N = (int)H;
+    gh.A = W; gh.lda = H; gh.M = (int)H;
+    gh.B = ez; gh.ldb = p.ez_kp; gh.N = rows;
     gh.K = (int)V;
     gh.splits = p.dh_splits; gh.k_per_split = (int)p.dh_kps;
     gh.group_m = 4;
@@ -321,7 +318,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     gh.n_valid = nvalid; gh.mean = mean;
     {
     KernelTimer t(T_DH, s);
-    if (launch_gemm<T, EPI_STORE, false, true>(gh, s) != hipSuccess) return LCE_ERR_HIP;
+    if (launch_gemm<T, EPI_STORE, A_MN>(gh, s) != hipSuccess) return LCE_ERR_HIP;
     if (dx32) {
       const int64_t count = (int64_t)rows * H;
       hipLaunchKernelGGL((split_reduce_kernel<float, T>), dim3((unsigned)cdiv(count / 4, 256)), dim3(256), 0, s, dhp,
@@ -335,9 +332,9 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     }
     }
 
-    // dW (+)= dZ_c^T . X_c  (A = dZ_c MN-contig over the vocabulary, B = X_c blocked over H).
+    // dW (+)= dZ_c^T . X_c  (A = dZ_c blocked, rows = vocabulary; B = X_c blocked over H).
     GemmArgs gw{};
-    gw.A = ez; gw.lda = p.Vp; gw.M = (int)V;
+    gw.A = ez; gw.lda = p.ez_kp; gw.M = (int)V;
     gw.B = xm; gw.ldb = p.xm_kp; gw.N = (int)H;
     gw.K = rows;
     gw.splits = 1; gw.k_per_split = (int)round_up(rows, kTileBytes / p.esz);
@@ -356,17 +353,17 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
         hook->row0[b + 1] = r1;
         if (r1 > r0) {
           GemmArgs gb = gw;
-          gb.A = ez + r0;               // MN-contiguous over the vocabulary: rows r0.. of dZ^T
+          gb.A = ez + 32 * r0;          // blocked: vocabulary id r0 starts 32 r0 elements in
           gb.M = (int)(r1 - r0);
           gb.out = dW + r0 * H;
           KernelTimer t(T_DW, s);
-          if (launch_gemm<T, EPI_DW, true, true, false, true>(gb, s) != hipSuccess) return LCE_ERR_HIP;
+          if (launch_gemm<T, EPI_DW, A_BLK>(gb, s) != hipSuccess) return LCE_ERR_HIP;
         }
         if (hipEventRecord(hook->dw_done[b], s) != hipSuccess) return LCE_ERR_HIP;
       }
     } else {
     KernelTimer t(T_DW, s);
-    if (launch_gemm<T, EPI_DW, true, true, false, true>(gw, s) != hipSuccess) return LCE_ERR_HIP;
+    if (launch_gemm<T, EPI_DW, A_BLK>(gw, s) != hipSuccess) return LCE_ERR_HIP;
     }
   }
 

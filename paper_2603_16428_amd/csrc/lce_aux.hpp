@@ -99,60 +99,55 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   }
 }
 
-// dlogits, in place. For token i of the chunk and vocabulary id v (slice t = v / 128):
+// dlogits, in place, on e's blocked layout: fragment (jb, q), 1 KB at byte (jb KP + q) 1024, holds
+// tokens 32 jb .. 32 jb + 31 by the q-th 32 bytes of the vocabulary; lane l's 16 bytes are token
+// 32 jb + l%32, ids from (32 q + 16 (l/32)) / sizeof(T). For token i of the chunk and id v
+// (slice t = v / 128):
 //   dZ[i][v] = g_i exp(m_t,i - lse_i) e[i][v] - g_i [v == y_i],   g_i = valid_i / n_valid (mean) or valid_i,
-// where e = exp(z - m_t,i) was stored by the logits GEMM. Entries outside the valid tokens and
-// vocabulary but inside the pitches are written as zeros (the dH GEMM reads the vocabulary padding
-// of each row). One block per 64 tokens x 128 ids; 16-byte accesses. For fp16 both e and dZ carry
-// the storage scales of Storage<f16> (dZ = (p - onehot) kDz for valid tokens; g is applied later).
+// where e = exp(z - m_t,i) was stored by the logits GEMM. Every piece of the buffer is written:
+// tokens at or beyond `rows` and ids at or beyond V as zeros (the dW GEMM sums over the last token
+// block, the dH GEMM reads the id padding). Block (b, jb) covers K-pairs 16 b .. 16 b + 15 of token
+// block jb (KP is a multiple of 16); wave w takes K-pairs 16 b + 4 w .. + 3, which lie in one
+// slice, so each lane has one token and one scale. For fp16 both e and dZ carry the storage
+// scales of Storage<f16> (dZ = (p - onehot) kDz for valid tokens; g is applied later).
 template <typename T>
-__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t ldz, const float* __restrict__ pmax,
+__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t KP, const float* __restrict__ pmax,
                                                       int64_t ldp, const float* __restrict__ lse,
                                                       const int64_t* __restrict__ y, int64_t ignore_index,
                                                       const int* __restrict__ n_valid, int mean, int rows,
                                                       int V) {
-  constexpr int kVec = 16 / sizeof(T);          // elements per 16-byte access
-  constexpr int kTpr = 128 / kVec;              // threads per 128-id row segment
-  constexpr int kRowsPerPass = 256 / kTpr;
-  const int v0 = blockIdx.x * 128, i0 = blockIdx.y * 64;
-  const int slice = blockIdx.x;
+  constexpr int kVec = 16 / sizeof(T);          // ids per piece
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int jb = blockIdx.y;
+  const int64_t q0 = 16 * (int64_t)blockIdx.x + 4 * w;
+  char* piece = (char*)ez + ((size_t)jb * KP + q0) * 1024 + l * 16;
+  // All four pieces are read before any is written: HBM needs the loads in flight together. Tokens
+  // at or beyond `rows` read stale data that the select below discards.
+  uint4 raw[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) raw[k] = *(const uint4*)(piece + k * 1024);
+  const int i = 32 * jb + (l & 31);
+  const int ic = min(i, rows - 1);
+  const int64_t lab = y[ic];
+  const bool active = i < rows && lab != ignore_index;
+  const int v0 = (int)((q0 * 32 + 16 * (l >> 5)) / (int)sizeof(T));
+  const int slice = min(v0, V - 1) / kLseSlice;
   const int nv = *n_valid;
   const float g = Storage<T>::kDzUnscaled ? Storage<T>::kDz : (mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f);
   constexpr float kInvE = 1.f / Storage<T>::kE;
-  constexpr int kPasses = 64 / kRowsPerPass;
-  const int tc = threadIdx.x % kTpr, tr = threadIdx.x / kTpr;
-  const int v = v0 + tc * kVec;
-  // All of the thread's rows are read, unconditionally, before any is written: stores to the same
-  // buffer, or loads under a branch, would leave one load in flight per thread, and HBM needs
-  // more. Rows at or beyond `rows` (inside the chunk's padded rows, so in bounds) read stale data
-  // that the select below discards; labels and lse are read at a clamped row.
-  uint4 raw[kPasses];
-  float c[kPasses];
-  bool active[kPasses];
+  const float c = g * kInvE * __expf(pmax[(size_t)slice * ldp + i] - lse[ic]);
 #pragma unroll
-  for (int q = 0; q < kPasses; ++q) {
-    const int i = i0 + tr + q * kRowsPerPass;
-    const int ic = min(i, rows - 1);
-    const int64_t lab = y[ic];
-    const float pm = pmax[(size_t)slice * ldp + i];
-    const float ls = lse[ic];
-    raw[q] = *(const uint4*)(ez + (size_t)i * ldz + v);
-    active[q] = i < rows && lab != ignore_index;
-    c[q] = g * kInvE * __expf(pm - ls);
-  }
-#pragma unroll
-  for (int q = 0; q < kPasses; ++q) {
-    const int i = i0 + tr + q * kRowsPerPass;
-    const int64_t lab = y[min(i, rows - 1)];
+  for (int k = 0; k < 4; ++k) {
+    const int v = v0 + k * (32 / (int)sizeof(T));
     T ev[kVec], outv[kVec];
-    *(uint4*)ev = raw[q];
+    *(uint4*)ev = raw[k];
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
-      float d = (active[q] && v + e < V) ? c[q] * to_f32(ev[e]) : 0.f;
-      if (active[q] && v + e == lab) d -= g;
+      float d = (active && v + e < V) ? c * to_f32(ev[e]) : 0.f;
+      if (active && v + e == lab) d -= g;
       outv[e] = from_f32<T>(d);
     }
-    *(uint4*)(ez + (size_t)i * ldz + v) = *(const uint4*)outv;
+    *(uint4*)(piece + k * 1024) = *(const uint4*)outv;
   }
 }
 

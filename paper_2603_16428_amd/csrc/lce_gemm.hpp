@@ -2,47 +2,41 @@
 //
 //   C[m, n] = sum_k A(m, k) * B(n, k)
 //
-// Each operand is stored either K-contiguous (element (m, k) at P[m * ld + k]) or MN-contiguous
-// (element (m, k) at P[k * ld + m]). The three contractions use:
-//   logits^T = W . X_c^T     A = W [V, H] K-contig,        B = X_c [n_c, H] K-contig
-//   dH_c     = dZ_c . W      A = dZ_c [n_c, V] K-contig,   B = W [V, H] MN-contig
-//   dW      += dZ_c^T . X_c  A = dZ_c [n_c, V] MN-contig,  B = X_c [n_c, H] MN-contig
-// so W and dZ are never transposed in memory. Two main loops share the tile, waves, fragment
-// reads and epilogues: gemm_kernel (below) takes both operands through LDS and runs dH;
-// gemm_xb_kernel (at the end of this file) reads B from a fragment-blocked copy straight into
-// registers and runs the logits and dW contractions, whose B is the small X chunk.
+// Operand A is stored K-contiguous (element (m, k) at P[m * ld + k]), MN-contiguous (element
+// (m, k) at P[k * ld + m]) or fragment-blocked; operand B is always fragment-blocked (the layout is
+// defined above gemm_xb_kernel). The three contractions use:
+//   logits^T = W . X_c^T      A = W [V, H] K-contig,    B = X_c blocked (columns tokens, K = H)
+//   dH_c^T   = W^T . dZ_c^T   A = W [V, H] MN-contig,   B = dZ_c blocked (columns tokens, K = V)
+//   dW      += dZ_c^T . X_c   A = dZ_c blocked,         B = X_c blocked (columns H, K = tokens)
+// The logits epilogue stores e, and dlogits then dZ, in the blocked layout itself, so W is never
+// transposed or copied and only the small X chunk is rearranged (twice per chunk).
 //
-// gemm_kernel. One workgroup computes a 256 x 256 tile of C with four waves (2 x 2), each wave a
-// 128 x 128 sub-tile held as 4 x 4 blocks of the 32x32 MFMA accumulator (256 fp32 per lane). K
-// advances in K-tiles of 64 bf16 (32 fp32); an operand's K-tile is 32 KB of LDS either way:
-// 256 rows of 128 bytes (K-contig) or 64 (32) K-rows of 512 (1024) bytes (MN-contig). Global loads
-// are 16 bytes per lane and read whole 128-byte lines.
+// One workgroup computes a 256 x 256 tile of C with four waves (2 x 2), each wave a 128 x 128
+// sub-tile held as 4 x 4 blocks of the 32x32 MFMA accumulator (256 fp32 per lane). K advances in
+// K-tiles of 64 bf16 (32 fp32); A's K-tile is 32 KB of LDS either way: 256 rows of 128 bytes
+// (K-contig) or 64 (32) K-rows of 512 (1024) bytes (MN-contig and blocked). Global loads are 16
+// bytes per lane. Buffer descriptors turn rows beyond M (K-contig) or K-rows beyond the K range
+// (MN-contig and blocked, one descriptor per K-tile), and K-tiles past the end, into zeros.
 //
-// Every K-tile is requested about two K-tiles ahead of its MFMAs: with a single K-tile in flight per
-// CU the MFMAs wait on this access pattern's load latency, and three LDS stages of both operands
-// (192 KB) do not fit in the 160 KB of LDS. So operand A streams straight into a ring of three LDS
-// slots (buffer_load ... lds) while operand B is parked in one of two register buffers
-// (buffer_load_dwordx4, 64 VGPRs) and written (ds_write_b128) into one of two LDS slots during the
-// preceding K-tile. Buffer descriptors turn rows beyond M/N (K-contig) or K-rows beyond the K
-// range (MN-contig, one descriptor per K-tile), and K-tiles past the end, into zeros.
-//
-// Fragments: for the 32x32x16 bf16 MFMA a lane supplies 8 consecutive K of one row/column.
-// K-contig tiles give them with one ds_read_b128; MN-contig bf16 tiles with two ds_read_b64_tr_b16
-// (each 16-lane group reads four K-rows of 16 columns and the LDS transposes them so that lane j
+// A's fragments: for the 32x32x16 bf16 MFMA a lane supplies 8 consecutive K of one row. K-contig
+// tiles give them with one ds_read_b128; MN-contig bf16 tiles with two ds_read_b64_tr_b16 (each
+// 16-lane group reads four K-rows of 16 columns and the LDS transposes them so that lane j
 // receives column j of the four rows); MN-contig fp32 tiles with four ds_read_b32. The 16-byte
-// slots of every LDS row are XOR-swizzled so that these reads are free of bank conflicts.
-// Fragments are double-buffered in registers: the reads for the next 32 bytes of K are in flight
-// while the MFMAs of the current ones run.
+// slots of every LDS row are XOR-swizzled so that these reads are free of bank conflicts. A
+// blocked A is fetched into the very LDS slots an MN-contig one would occupy. Fragments are
+// double-buffered in registers: the reads for the next 32 bytes of K are in flight while the
+// MFMAs of the current ones run.
 //
 // The epilogue decides what the tile becomes:
 //   LSE_FWD / LSE_BWD : C = logits^T tile (rows = vocabulary, columns = tokens). Per token and per
 //                       128-row vocabulary slice: the maximum m and sum exp(z - m) (the vocabulary-
-//                       tiled online log-sum-exp); LSE_BWD also stores e = exp(z - m) token-major.
-//   STORE             : C written as the output dtype (or as fp32 split-K partials).
+//                       tiled online log-sum-exp); LSE_BWD also stores e = exp(z - m), blocked.
+//   STORE             : C^T written token-major as the output dtype (or as fp32 split-K partials):
+//                       the chunk's dH rows from dH^T tiles.
 //   DW                : C written into dW (first chunk) or added to it (later chunks).
-// STORE and DW issue the MFMAs with the operands swapped, so each lane holds four consecutive
-// columns of C (LSE_BWD: four consecutive vocabulary rows of e's token-major row). bf16 results
-// are regrouped between lanes l and l + 32 so that each store writes 32 contiguous bytes per row.
+// DW issues the MFMAs with the operands swapped, so each lane holds four consecutive columns of C;
+// LSE and STORE keep four consecutive rows of C (vocabulary ids, hidden units) per lane. 16-bit
+// results are regrouped between lanes l and l + 32 so that each lane stores 16 contiguous bytes.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -68,17 +62,14 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr int kTile = 256;                       // BM = BN
 constexpr int kTileBytes = 128;                  // bytes of K per row of a K-contig K-tile
 constexpr int kOperandBytes = 32 * 1024;         // one operand's K-tile in LDS
-constexpr int kASlots = 3;                       // A: ring of K-tiles filled by LDS-DMA
-constexpr int kBSlots = 2;                       // B: LDS slots filled from registers
-constexpr int kBBase = kASlots * kOperandBytes;  // B slots follow the A ring
-constexpr int kGemmSmem = (kASlots + kBSlots) * kOperandBytes;  // 160 KB, all of a CU's LDS
-constexpr int kLoadsPerOperand = 8;              // 16-byte loads per lane per operand K-tile
 constexpr int kGemmThreads = 256;
 constexpr int kLseSlice = 128;                   // vocabulary rows per log-sum-exp partial
 constexpr uint32_t kOOB = 0x80000000u;           // a buffer offset beyond every range check
 constexpr float kLog2e = 1.4426950408889634f;
 
 enum Epilogue { EPI_LSE_FWD = 0, EPI_LSE_BWD = 1, EPI_STORE = 2, EPI_DW = 3 };
+// Layouts of operand A: K-contiguous, MN-contiguous, fragment-blocked (MN pieces, see Operand).
+enum ALayout { A_K = 0, A_MN = 1, A_BLK = 2 };
 enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1 };
 
 struct GemmArgs {
@@ -89,8 +80,8 @@ struct GemmArgs {
   int tiles_m, tiles_n, splits, k_per_split;  // k_per_split: a multiple of the K-tile
   int group_m;        // tile rows per raster group
   // epilogue
-  void* out;          // LSE_BWD: e (token-major, pitch ldo >= M rounded up to 128); STORE: output or
-                      // fp32 partials; DW: dW
+  void* out;          // LSE_BWD: e, blocked (ldo = K-pairs per token block, covering M rounded up
+                      // to 256); STORE: token-major output or fp32 partials; DW: dW
   int64_t ldo;
   float* pmax;        // LSE: [slices, ldp]
   float* psum;
@@ -222,12 +213,6 @@ __device__ __forceinline__ float dz_epilogue_scale(const int* n_valid, int mean)
   }
 }
 
-// A 16-bit output row segment of 32 elements held by lanes l and l + 32 (half = l / 32): lane l has
-// the 4-element groups at 8q + 4 half, q = 0..3, as v[4q + e]. One v_permlane32_swap per dword
-// regroups them so that lane l ends with elements 0-7 and 16-23 and lane l + 32 with 8-15 and
-// 24-31, and each store instruction writes 32 contiguous bytes of the row instead of 16 (the
-// stores of a tile's epilogue are a burst that every CU issues at about the same time).
-// in0 / in1: whether this lane's first / second 8 elements lie inside the output.
 // The lane index, recomputed where it is needed: values derived from it early and kept alive
 // through the main loop for the epilogue would be spilled.
 __device__ __forceinline__ int lane_id() {
@@ -236,10 +221,14 @@ __device__ __forceinline__ int lane_id() {
   return (int)ln;
 }
 
+// A 16-bit segment of 32 consecutive elements held by lanes l and l + 32 (half = l / 32): lane l
+// has the 4-element groups at 8q + 4 half, q = 0..3, as v[4q + e]. One v_permlane32_swap per dword
+// regroups them so that lane l ends with elements 0-7 (lo) and 16-23 (hi) and lane l + 32 with
+// 8-15 and 24-31: whole 16-byte pieces, so that each store instruction writes 32 contiguous bytes
+// of a row instead of 16, or one whole 1 KB fragment of the blocked layout.
 template <typename T>
-__device__ __forceinline__ void store_row32(T* p, const f32x16& v, bool in0, bool in1) {
+__device__ __forceinline__ void regroup32(const f32x16& v, u32x4& lo, u32x4& hi) {
   typedef T t4 __attribute__((ext_vector_type(4)));
-  const int half = lane_id() >> 5;
   uint32_t a[4], b[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -256,16 +245,49 @@ __device__ __forceinline__ void store_row32(T* p, const f32x16& v, bool in0, boo
     a[e] = r[0];
     b[e] = r[1];
   }
-  if (in0) *(u32x4*)(p + 8 * half) = (u32x4){a[0], a[1], b[0], b[1]};
-  if (in1) *(u32x4*)(p + 16 + 8 * half) = (u32x4){a[2], a[3], b[2], b[3]};
+  lo = (u32x4){a[0], a[1], b[0], b[1]};
+  hi = (u32x4){a[2], a[3], b[2], b[3]};
 }
 
-// Loads and fragment reads of one operand (the tile's 256 rows/columns starting at mn0).
-template <typename T, bool MN>
+// Row-major: the segment starts at p; in0 / in1: whether this lane's first / second 8 elements lie
+// inside the output.
+template <typename T>
+__device__ __forceinline__ void store_row32(T* p, const f32x16& v, bool in0, bool in1) {
+  const int half = lane_id() >> 5;
+  u32x4 lo, hi;
+  regroup32<T>(v, lo, hi);
+  if (in0) *(u32x4*)(p + 8 * half) = lo;
+  if (in1) *(u32x4*)(p + 16 + 8 * half) = hi;
+}
+
+// Blocked: the segment is 32 vocabulary ids of one token, which fill this lane's 16-byte piece of
+// two consecutive fragments; p is the piece in the first.
+template <typename T>
+__device__ __forceinline__ void store_frag32(char* p, const f32x16& v) {
+  u32x4 lo, hi;
+  regroup32<T>(v, lo, hi);
+  *(u32x4*)p = lo;
+  *(u32x4*)(p + 1024) = hi;
+}
+
+// Loads and fragment reads of operand A (the tile's 256 rows starting at mn0) in layout AL.
+//
+// Blocked A (AL = A_BLK) is dZ as the logits epilogue and dlogits leave it: M = vocabulary ids,
+// K = tokens, in the fragment-blocked layout with the tokens as its columns and the ids as its K
+// (ld = K-pairs per 32-token block). Element (m, k) is at byte (k / 32 ld + m s / 32) 1024 +
+// (k % 32 + 32 ((m s / 16) % 2)) 16 + (m s) % 16, s = sizeof(T): a 16-byte piece holds 16 / s
+// consecutive ids of one token. 16-bit: each load fetches one whole fragment (1 KB, 32 tokens by
+// 16 ids) into LDS as it is, up to a permutation of its pieces, and the transposing fragment reads
+// find each lane's four ids of a token inside a piece. fp32: each load fetches the MN-contig
+// pieces (4 ids of one token at 512 c + 16 (k % 32) past the token block's start of the tile's
+// ids, c the MN slot), 32 scattered pieces per load, into the MN-contig LDS layout.
+template <typename T, int AL>
 struct Operand {
   static constexpr int kEsz = (int)sizeof(T);
   static constexpr int kBK = kTileBytes / kEsz;       // K per K-tile
   static constexpr int kMnRowBytes = kTile * kEsz;    // MN-contig: bytes per K-row
+  static constexpr bool MN = AL != A_K;                // the MN-contig LDS layout and fragment reads
+  static constexpr bool BLK = AL == A_BLK;
 
   const char* base;   // element (mn0, 0)
   int64_t ld;
@@ -295,27 +317,53 @@ struct Operand {
 #pragma unroll
       for (int i = 0; i < 4; ++i) frag[i] = (wsub + 32 * i + (lane & 31)) * kTileBytes;
     } else {
-      base = (const char*)p + (size_t)mn0 * kEsz;
+      base = BLK ? (const char*)p + (size_t)mn0 * 32 * kEsz : (const char*)p + (size_t)mn0 * kEsz;
       if constexpr (kEsz == 2) {
-        // Load j of wave w: lane l holds K-row kr = 16w + 2j + l/32, slot l%32, which is logical
-        // slot (l%32) ^ swz_mn(kr), and swz_mn(kr) = 4 (l/32) ^ 10 (j&1) ^ 16 ((j>>2)&1).
-        row_off = (uint32_t)(16 * w + (lane >> 5)) * (uint32_t)ld * 2;
-        row_step = 2u * (uint32_t)ld * 2;
-        slot_x = (uint32_t)(((lane & 31) ^ (4 * (lane >> 5))) << 4);
-        // Transposed reads: 16-lane group g, lane i' = l%16 reads K-row 16p + 8(g/2) + 4s + i'/4
-        // at column wsub + 32i + 16(g%2) + 4(i'%4). The swizzle depends only on row bits 0, 1
-        // and 3, all fixed by the lane, so the address is this base plus (16p + 4s) * 512.
-        // Block i only flips address bits 6-7: its 16-byte slot is block 0's XOR 4i (the column's
-        // slot bits 2-3 come from 32i alone), so frag[i] = frag[0] ^ (i << 6).
         const int g = lane >> 4, ip = lane & 15;
-        const int r0 = 8 * (g >> 1) + (ip >> 2);
-        const int col = wsub + 16 * (g & 1) + 4 * (ip & 3);
-        frag[0] = r0 * kMnRowBytes + (((col >> 3) ^ swz_mn(r0)) << 4) + 8 * ((col >> 2) & 1);
+        if constexpr (BLK) {
+          // The LDS K-tile holds the 32 fragments of the K-tile's two token blocks b by the
+          // tile's 16 id fragments c, fragment (b, c) in 1 KB slot 16 b + c. Piece P of a fragment
+          // (token P%32, id half P/32) sits at 16 Q, Q = P ^ 4 (P/32) ^ 8 (c%2), so that the
+          // fragment reads below are free of bank conflicts. Load j of wave w fills slot 8w + j:
+          // token block w/2, c = 8 (w%2) + j; lane l fetches piece l ^ 4 (l/32) ^ 8 (j%2).
+          row_off = (uint32_t)(w >> 1) * (uint32_t)ld * 1024u + (uint32_t)(w & 1) * 8192u;
+          row_step = 1024u;
+          slot_x = (uint32_t)((lane ^ (4 * (lane >> 5))) << 4);
+          // Transposed reads: 16-lane group g, lane i' = l%16 reads token 16p + 8(g/2) + 4s + i'/4
+          // of the K-tile, ids wsub + 32i + 16(g%2) + 4(i'%4) .. + 3: slot 16 (p/2) + (wsub +
+          // 32i)/16 + g%2, Q = i'/4 + 4 (s ^ h) + 8 ((g/2) ^ (g%2)) + 16 (p%2) + 32 h with
+          // h = (i'%4)/2, byte 8 (i'%2) of the piece. frag[0] is the address at p = s = i = 0;
+          // s flips bit 6, p and i add 16384 (p/2) + 256 (p%2) + 2048 i.
+          const int h = (ip & 3) >> 1;
+          frag[0] = (wsub / 16 + (g & 1)) * 1024 + 16 * ((ip >> 2) + 4 * h + 8 * ((g >> 1) ^ (g & 1)) + 32 * h) +
+                    8 * (ip & 1);
+        } else {
+          // Load j of wave w: lane l holds K-row kr = 16w + 2j + l/32, slot l%32, which is logical
+          // slot (l%32) ^ swz_mn(kr), and swz_mn(kr) = 4 (l/32) ^ 10 (j&1) ^ 16 ((j>>2)&1).
+          row_off = (uint32_t)(16 * w + (lane >> 5)) * (uint32_t)ld * 2;
+          row_step = 2u * (uint32_t)ld * 2;
+          slot_x = (uint32_t)(((lane & 31) ^ (4 * (lane >> 5))) << 4);
+          // Transposed reads: 16-lane group g, lane i' = l%16 reads K-row 16p + 8(g/2) + 4s + i'/4
+          // at column wsub + 32i + 16(g%2) + 4(i'%4). The swizzle depends only on row bits 0, 1
+          // and 3, all fixed by the lane, so the address is this base plus (16p + 4s) * 512.
+          // Block i only flips address bits 6-7: its 16-byte slot is block 0's XOR 4i (the column's
+          // slot bits 2-3 come from 32i alone), so frag[i] = frag[0] ^ (i << 6).
+          const int r0 = 8 * (g >> 1) + (ip >> 2);
+          const int col = wsub + 16 * (g & 1) + 4 * (ip & 3);
+          frag[0] = r0 * kMnRowBytes + (((col >> 3) ^ swz_mn(r0)) << 4) + 8 * ((col >> 2) & 1);
+        }
       } else {
         // fp32: load j of wave w: lane l holds K-row 8w + j, slot l; fragment reads are plain.
-        row_off = (uint32_t)(8 * w) * (uint32_t)ld * 4;
-        row_step = (uint32_t)ld * 4;
-        slot_x = (uint32_t)(lane * 16);
+        // Blocked: K-row 8w + j is token 8w + j of the K-tile's one token block; slot l at 512 l.
+        if constexpr (BLK) {
+          row_off = (uint32_t)(8 * w) * 16u;
+          row_step = 16u;
+          slot_x = (uint32_t)lane << 9;
+        } else {
+          row_off = (uint32_t)(8 * w) * (uint32_t)ld * 4;
+          row_step = (uint32_t)ld * 4;
+          slot_x = (uint32_t)(lane * 16);
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) frag[i] = (4 * (lane >> 5)) * kMnRowBytes + (wsub + 32 * i + (lane & 31)) * 4;
       }
@@ -325,15 +373,27 @@ struct Operand {
   // The compile-time XOR part of load j's offset.
   static __device__ __forceinline__ constexpr uint32_t xor_j(int j) {
     if constexpr (!MN) return (uint32_t)(j << 4);
+    else if constexpr (kEsz == 2 && BLK) return (uint32_t)((j & 1) ? 128 : 0);
     else if constexpr (kEsz == 2) return (uint32_t)((((j & 1) ? 10 : 0) ^ (((j >> 2) & 1) ? 16 : 0)) << 4);
     else return 0u;
   }
 
   // Descriptor for K-tile t. MN-contig: its valid K-rows only, so that rows at or beyond ke,
-  // including whole K-tiles past the end, read zeros without touching memory.
+  // including whole K-tiles past the end, read zeros without touching memory. Blocked: the token
+  // blocks that hold tokens below ke (the rest of the last one is zeros in memory), up to the end
+  // of the tile's ids in the last of them.
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(int t) const {
     if constexpr (!MN) {
       return rsrc_k;
+    } else if constexpr (BLK) {
+      // Branch-free (a branch here would split the main loop's scheduled sections): a K-tile at or
+      // past the end gets no blocks and an empty range, whatever its base.
+      const int k0 = kb + t * kBK;
+      const int nblk = min(kBK / 32, (max(ke - k0, 0) + 31) >> 5);
+      const uint32_t blk = (uint32_t)ld * 1024u;
+      const uint32_t bytes = (uint32_t)nblk * blk - (uint32_t)min(nblk, 1) * (blk - (uint32_t)(kTile * kEsz * 32));
+      const char* p = base + (size_t)(k0 >> 5) * blk;
+      return make_rsrc((const void*)uniform64((uint64_t)p), __builtin_amdgcn_readfirstlane(bytes));
     } else {
       const int k0 = kb + t * kBK;
       const int nrows = max(0, min(kBK, ke - k0));
@@ -385,6 +445,20 @@ struct Operand {
   __device__ __forceinline__ f32x4 fragment(const char* st, int p, int i, int khalf, int sw) const {
     if constexpr (!MN) {
       return *(const f32x4*)(st + frag[i] + (((2 * p + khalf) ^ sw) << 4));
+    } else if constexpr (kEsz == 2 && BLK) {
+      // As below; the two reads of a fragment differ in address bit 6 (s), which the tile base
+      // (a multiple of 1 KB) leaves alone, and p and i only add an immediate offset.
+      i16x4 lo, hi;
+      uint32_t a, b;
+      asm volatile(
+          "v_add_u32 %2, %4, %5\n\t"
+          "v_xor_b32 %3, 64, %2\n\t"
+          "ds_read_b64_tr_b16 %0, %2 offset:%6\n\t"
+          "ds_read_b64_tr_b16 %1, %3 offset:%6"
+          : "=v"(lo), "=v"(hi), "=&v"(a), "=&v"(b)
+          : "s"((uint32_t)(uintptr_t)(lds_void*)st), "v"(frag[0]), "i"(16384 * (p >> 1) + 256 * (p & 1) + 2048 * i));
+      const i16x4 v[2] = {lo, hi};
+      return __builtin_bit_cast(f32x4, v);
     } else if constexpr (kEsz == 2) {
       // Issued as inline assembly: the compiler cannot tell which LDS bytes the transposing read
       // builtin touches, and so would wait for every outstanding LDS-DMA load before it. The
@@ -464,8 +538,9 @@ __device__ __forceinline__ float dw_prev_scale(const GemmArgs& g) {
 }
 
 // The epilogue: what a wave's 128 x 128 accumulator sub-tile at (mw, nw) becomes. Without the
-// operand swap, accumulator element r of block (i, j) sits at row = 32i + 8(r/4) + 4(l/32) + r%4,
-// col = 32j + l%32 of the sub-tile; with it, at row = 32i + l%32, col = 32j + 8(r/4) + 4(l/32) + r%4.
+// operand swap (LSE, STORE), accumulator element r of block (i, j) sits at row = 32i + 8(r/4) +
+// 4(l/32) + r%4, col = 32j + l%32 of the sub-tile; with it (DW), at row = 32i + l%32,
+// col = 32j + 8(r/4) + 4(l/32) + r%4.
 // PRELOADED (DW): the accumulators started from the tile's current dW values.
 template <typename T, int EPI, bool PRELOADED>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4][4], int mw, int nw, int split,
@@ -503,12 +578,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
       s += __shfl_xor(s, 32);
       if (col < g.N) {
         if constexpr (EPI == EPI_LSE_BWD) {
-          T* e_row = (T*)g.out + (size_t)col * g.ldo;
+          // e blocked: the token is column l%32 of token block col/32, so this lane's piece of every
+          // fragment of that block is at lane * 16; 32 ids fill the lane's pieces of two fragments.
+          char* e_blk = (char*)g.out + (size_t)((nw + 32 * j) >> 5) * g.ldo * 1024 + lane * 16;
           if constexpr (kEsz == 2) {
-            // Whole 128-row wave slices: e's pitch is M rounded up to 128, and rows at or beyond M
-            // hold exp = 0 here.
+            // Whole 128-row wave slices: the blocked rows cover M rounded up to 256, and rows at or
+            // beyond M hold exp = 0 here.
 #pragma unroll
-            for (int i = 0; i < 4; ++i) store_row32(e_row + mw + 32 * i, acc[i][j], true, true);
+            for (int i = 0; i < 4; ++i) store_frag32<T>(e_blk + (size_t)((mw + 32 * i) >> 4) * 1024, acc[i][j]);
           } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -516,8 +593,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
               for (int q = 0; q < 4; ++q) {
                 const int row = mw + 32 * i + 8 * q + sub4;
                 if (row < g.M)
-                  store4(e_row + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                         acc[i][j][4 * q + 3]);
+                  store4((T*)(e_blk + (size_t)((mw + 32 * i + 8 * q) >> 3) * 1024), acc[i][j][4 * q],
+                         acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
               }
           }
         }
@@ -527,47 +604,56 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
         }
       }
     }
+  } else if constexpr (EPI == EPI_STORE) {
+    // C^T token-major: column n = nw + 32j + l%32 of C is row n of the output, and the lane's four
+    // consecutive rows of C per (i, q) are four consecutive elements of it. M (the output's row
+    // length) is a multiple of 8 for 16-bit types and of 4 for fp32, so pieces are all in or out.
+    // mode 1: fp32 partials, split s at out + s * N * ldo.
+    const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = nw + 32 * j + l32;
+      if (col >= g.N) continue;
+      if (g.mode == 1) {
+        float* o = (float*)g.out + ((size_t)split * g.N + col) * g.ldo;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = mw + 32 * i + 8 * q + sub4;
+            if (row < g.M)
+              store4(o + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          }
+      } else {
+        T* o = (T*)g.out + (size_t)col * g.ldo;
+        if constexpr (kEsz == 2) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if constexpr (Storage<T>::kDzUnscaled) acc[i][j] *= sc;
+            const int r0 = mw + 32 * i + 8 * (lane >> 5);
+            store_row32(o + mw + 32 * i, acc[i][j], r0 < g.M, r0 + 16 < g.M);
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int row = mw + 32 * i + 8 * q + sub4;
+              if (row < g.M)
+                store4(o + row, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+            }
+        }
+      }
+    }
   } else {
-    // Swapped layout: lane owns rows mw + 32i + l%32 and 4 consecutive columns per (j, q).
+    // DW, swapped layout: lane owns rows mw + 32i + l%32 and 4 consecutive columns per (j, q).
     // N (the output pitch) is a multiple of 4 here, so a 4-column group is all in or all out.
     const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = mw + 32 * i + l32;
       if (row >= g.M) continue;
-      if constexpr (EPI == EPI_STORE) {
-        if (g.mode == 1) {
-          float* o = (float*)g.out + (size_t)split * g.M * g.ldo + (size_t)row * g.ldo;
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int col = nw + 32 * j + 8 * q + sub4;
-              if (col < g.N)
-                store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-            }
-        } else {
-          T* o = (T*)g.out + (size_t)row * g.ldo;
-          if constexpr (kEsz == 2) {
-            // N is a multiple of 8 for 16-bit types, so an 8-column piece is all in or all out.
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              if constexpr (Storage<T>::kDzUnscaled) acc[i][j] *= sc;
-              const int c0 = nw + 32 * j + 8 * (lane >> 5);
-              store_row32(o + nw + 32 * j, acc[i][j], c0 < g.N, c0 + 16 < g.N);
-            }
-          } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const int col = nw + 32 * j + 8 * q + sub4;
-                if (col < g.N)
-                  store4(o + col, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              }
-          }
-        }
-      } else if constexpr (PRELOADED) {  // EPI_DW, 16-bit: the accumulators already hold the earlier chunks' sum
+      if constexpr (PRELOADED) {  // EPI_DW, 16-bit: the accumulators already hold the earlier chunks' sum
         T* o = (T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -598,216 +684,22 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
   }
 }
 
-// KCHECK: K-contig operands check every chunk against the K range (see Operand::offset).
-template <typename T, int EPI, bool A_MN, bool B_MN, bool KCHECK>
-__global__ __launch_bounds__(kGemmThreads, 1) void gemm_kernel(const GemmArgs g) {
-  extern __shared__ __attribute__((aligned(1024))) char smem[];
-  constexpr int kEsz = (int)sizeof(T);
-  constexpr int kBK = kTileBytes / kEsz;   // elements per K-tile
-  constexpr bool kSwap = (EPI == EPI_STORE || EPI == EPI_DW);
-
-  const int lane = threadIdx.x & 63;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = w >> 1, wn = w & 1;
-
-  const int total = g.tiles_m * g.tiles_n * g.splits;
-  int tm, rest;
-  tile_coords(blockIdx.x, total, g.tiles_m, g.group_m, tm, rest);
-  tm = __builtin_amdgcn_readfirstlane(tm);
-  rest = __builtin_amdgcn_readfirstlane(rest);
-  const int tn = rest % g.tiles_n;
-  const int split = rest / g.tiles_n;
-  const int m0 = tm * kTile, n0 = tn * kTile;
-  const int kb = split * g.k_per_split;
-  const int ke = min(g.K, kb + g.k_per_split);
-
-  Operand<T, A_MN> opa;
-  Operand<T, B_MN> opb;
-  opa.init(g.A, g.lda, m0, min(kTile, g.M - m0), kb, ke, w, lane, wm * 128);
-  opb.init(g.B, g.ldb, n0, min(kTile, g.N - n0), kb, ke, w, lane, wn * 128);
-  const int khalf = lane >> 5;
-  // K-contig fragments: swz_k(row) depends on row % 64 only, the same for a lane's A and B rows.
-  int swi[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) swi[i] = swz_k(i * 32 + (lane & 31));
-
-  // A K-tile t: LDS-DMA into ring slot t % 3.
-  auto load_a = [&](int t) {
-    const __amdgpu_buffer_rsrc_t r = opa.rsrc(t);
-    char* st = smem + (t % kASlots) * kOperandBytes + w * 8 * 1024;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if constexpr (KCHECK && !A_MN) dma16(r, st + j * 1024, opa.offset(t, j));
-      else dma16(r, st + j * 1024, opa.lane_offset(j), opa.uniform_offset(t, j));
-    }
-  };
-  // B K-tile t: into register buffer t % 2 (the caller passes that parity as a constant, so that
-  // the buffers stay in registers) ...
-  u32x4 vb[2][8];
-  auto load_b = [&](int t, auto par) {
-    const __amdgpu_buffer_rsrc_t r = opb.rsrc(t);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if constexpr (KCHECK && !B_MN) vb[par][j] = load16(r, opb.offset(t, j));
-      else vb[par][j] = load16(r, opb.lane_offset(j), opb.uniform_offset(t, j));
-    }
-  };
-  // ... then from there into LDS slot t % 2, at the same place LDS-DMA would have put it.
-  auto write_b = [&](auto par) {
-    char* st = smem + kBBase + par * kOperandBytes + w * 8 * 1024 + lane * 16;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) *(u32x4*)(st + j * 1024) = vb[par][j];
-  };
-  using P0 = std::integral_constant<int, 0>;
-  using P1 = std::integral_constant<int, 1>;
-
-  f32x16 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16){};
-
-  f32x4 fa[2][4], fb[2][4];
-  // Fragments of K-pair p of K-tile t into fragment buffer `buf`.
-  auto read_frags = [&](int t, int p, int buf) {
-    const char* sa = smem + (t % kASlots) * kOperandBytes;
-    const char* sb = smem + kBBase + (t & 1) * kOperandBytes;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa[buf][i] = opa.fragment(sa, p, i, khalf, swi[i]);
-      fb[buf][i] = opb.fragment(sb, p, i, khalf, swi[i]);
-    }
-  };
-  // Fragment reads issued as inline assembly are invisible to the compiler's wait insertion: at
-  // the start of each section wait for all earlier LDS traffic (the previous section's reads, long
-  // since done), with the fragment registers as operands so that no MFMA moves above the wait.
-  auto sync_frags = [&]() {
-    if constexpr ((A_MN || B_MN) && kEsz == 2) {
-      asm volatile("s_waitcnt lgkmcnt(0)"
-                   : "+v"(fa[0][0]), "+v"(fa[0][1]), "+v"(fa[0][2]), "+v"(fa[0][3]), "+v"(fb[0][0]),
-                     "+v"(fb[0][1]), "+v"(fb[0][2]), "+v"(fb[0][3]), "+v"(fa[1][0]), "+v"(fa[1][1]),
-                     "+v"(fa[1][2]), "+v"(fa[1][3]), "+v"(fb[1][0]), "+v"(fb[1][1]), "+v"(fb[1][2]),
-                     "+v"(fb[1][3])
-                   :
-                   : "memory");
-    }
-  };
-  auto mma = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if constexpr (kSwap) mfma_pair<T>(acc[i][j], fb[buf][j], fa[buf][i]);
-        else mfma_pair<T>(acc[i][j], fa[buf][i], fb[buf][j]);
-      }
-  };
-
-  // Main loop, one K-tile per iteration. On entry to iteration kt: A K-tile kt and B K-tile kt are
-  // in LDS, A K-tile kt + 1 and B K-tiles kt + 1, kt + 2 are in flight. Section p runs the 16
-  // MFMAs of K-pair p on fragments read during the previous section while the fragments of K-pair
-  // p + 1 are read. Section 0 also starts A K-tile kt + 2 (into the ring slot freed by the previous
-  // barrier); section 2 writes B K-tile kt + 1 into the other B slot and reloads its register
-  // buffer with B K-tile kt + 3. Then barrier, and section 3 reads K-pair 0 of K-tile kt + 1.
-  // Loads retire in issue order, which per iteration is A(kt + 2), B(kt + 3); the prologue issues
-  // B(0) A(0) B(1) A(1) B(2) so that "the K-tile needed next has landed" is always "at most 24
-  // loads outstanding". The scheduling-group hints pin the interleaving; fragment reads precede
-  // LDS-bound loads in program order (the compiler keeps LDS reads before LDS writes that follow).
-  constexpr int kAfter = 3 * kLoadsPerOperand;
-  constexpr int kReads = (A_MN ? 0 : 4) + (B_MN ? 0 : 4);  // compiler-visible LDS reads per K-pair
-  auto sched = [](int n_ds_write, int n_vmem) {
-    if constexpr (kEsz != 2) return;  // fp32: four MFMAs per K-pair; left to the compiler
-    // The section's LDS reads go one after each of its first MFMAs.
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                  // one MFMA
-      if (i < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                 // one LDS read
-      if (i < n_ds_write) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);             // one LDS write
-      if (i >= 16 - n_vmem) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);           // one global load
-    }
-    __builtin_amdgcn_sched_barrier(0);  // each section is scheduled on its own
-  };
-  // One iteration for K-tile kt, whose parity is `par` (a constant).
-  auto iteration = [&](int kt, auto par) {
-    constexpr int q = decltype(par)::value ^ 1;
-    sync_frags();
-    read_frags(kt, 1, 1);
-    load_a(kt + 2);
-    mma(0);
-    sched(0, kLoadsPerOperand);
-    sync_frags();
-    read_frags(kt, 2, 0);
-    mma(1);
-    sched(0, 0);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kAfter) : "memory");  // B(kt + 1) landed
-    sync_frags();
-    read_frags(kt, 3, 1);
-    write_b(std::integral_constant<int, q>{});
-    load_b(kt + 3, std::integral_constant<int, q>{});
-    mma(0);
-    sched(kLoadsPerOperand, kLoadsPerOperand);
-    // A(kt + 1) landed (vmcnt) for every wave (barrier); every wave wrote B(kt + 1) and finished
-    // reading the slots that the next iteration refills (lgkmcnt before the barrier).
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAfter) : "memory");
-    read_frags(kt + 1, 0, 0);
-    mma(1);
-    sched(0, 0);
-  };
-  // 16-bit dW accumulation (chunks after the first): the tile's current dW values are loaded here,
-  // raw, in flight together with the loads that fill the pipeline, and become the accumulators'
-  // starting values, so the epilogue only stores. (fp32 adds them in the epilogue instead: its
-  // 256 values per lane would not fit next to the pipeline's registers.)
-  const int mw = m0 + wm * 128, nw = n0 + wn * 128;
-  constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
-  const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
-  vec4_t<T> prev[kPreload ? 4 : 1][4][4];
-  if constexpr (kPreload) {
-    if (accumulate) load_dw_prev<T>(g, prev, mw, nw, lane);
-  }
-  // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
-  const int nk = (ke - kb + kBK - 1) / kBK;
-  if (nk > 0) {
-    load_b(0, P0{});
-    load_a(0);
-    load_b(1, P1{});
-    load_a(1);
-    if constexpr (kPreload) {
-      if (accumulate) apply_dw_prev<T>(acc, prev, dw_prev_scale<T>(g));
-    }
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsPerOperand) : "memory");  // B(0) landed
-    write_b(P0{});
-    load_b(2, P0{});
-    // A(0) landed and B(0) written, for every wave. (Not __syncthreads: it would also wait for
-    // every load in flight.)
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAfter) : "memory");
-    read_frags(0, 0, 0);
-    for (int kt = 0; kt < nk; kt += 2) {
-      iteration(kt, P0{});
-      iteration(kt + 1, P1{});
-    }
-    // Loads of K-tiles past the end may still be in flight (they target no memory); their LDS and
-    // registers must not be reused before they retire.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
-
-  gemm_epilogue<T, EPI, kPreload>(g, acc, mw, nw, split, accumulate);
-}
-
-// ---- Operand B straight to registers ---------------------------------------------------------
+// ---- The main loop: operand B straight to registers -------------------------------------------
 //
-// gemm_xb_kernel computes the same tile with the same waves and epilogues, but reads operand B from
-// a fragment-blocked copy straight into the registers the MFMAs take it from: every B load is one
-// whole 1 KB fragment, and B never passes through LDS, which halves a K-tile's LDS traffic (A's
-// 32 KB written, 64 KB read). A streams into a ring of four LDS slots by LDS-DMA, three K-tiles
-// ahead; B circulates through a ring of eight K-pairs of fragments (128 VGPRs), seven K-pairs ahead.
-// A K-tile is four sections of 16 MFMAs; each section issues one quarter of A's K-tile three ahead
-// (two LDS-DMA loads) and the four B fragments of the K-pair seven ahead, between its MFMAs.
+// gemm_xb_kernel reads operand B from its fragment-blocked layout straight into the registers the
+// MFMAs take it from: every B load is one whole 1 KB fragment, and B never passes through LDS, so
+// a K-tile's LDS traffic is A's alone (32 KB written, 64 KB read). A streams into a ring of four
+// LDS slots by LDS-DMA, three K-tiles ahead; B circulates through a ring of eight K-pairs of
+// fragments (128 VGPRs), seven K-pairs ahead. A K-tile is four sections of 16 MFMAs; each section
+// issues one quarter of A's K-tile three ahead (two LDS-DMA loads) and the four B fragments of the
+// K-pair seven ahead, between its MFMAs.
 //
-// Blocked layout of B (N columns, reduction K, element type T): fragment (jb, q) -- 32 columns by
+// Blocked layout (N columns, reduction K, element type T): fragment (jb, q) -- 32 columns by
 // K-pair q, the q-th 32 bytes of every column's K run -- is 1 KB at byte (jb KP + q) 1024, and lane
 // l of it holds column 32 jb + l%32, bytes [32 q + 16 (l/32), +16): the 16 bytes that lane feeds
-// the MFMA. KP counts the K-pairs per column block with K rounded up to a whole K-tile; columns at
-// or beyond N and K at or beyond K are zeros. (The A fragments read from LDS cover the same K bytes:
-// K-pair p of K-tile t, lane half h, bytes [32 p + 16 h, +16) of the K-tile.)
+// the MFMA. KP counts the K-pairs per column block with K rounded up to a whole K-tile at least;
+// columns at or beyond N and K at or beyond K are zeros. (The A fragments read from LDS cover the
+// same K bytes: K-pair p of K-tile t, lane half h, bytes [32 p + 16 h, +16) of the K-tile.)
 constexpr int kXbASlots = 4;
 constexpr int kXbAhead = kXbASlots - 1;
 constexpr int kXbSmem = kXbASlots * kOperandBytes;  // 128 KB
@@ -862,13 +754,16 @@ __global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src
   *(vec_t*)((char*)dst + ((size_t)jb * KP + q) * 1024 + l * 16) = v;
 }
 
-// g.B: the blocked copy of B; g.ldb: its KP. Splits must start at whole K-tiles (k_per_split).
-template <typename T, int EPI, bool A_MN, bool KCHECK>
+// g.A: operand A in layout AL (ALayout); g.B: operand B blocked, g.ldb its KP. KCHECK: a K-contig
+// A checks every chunk against the K range (see Operand::offset). Splits must start at whole
+// K-tiles (k_per_split).
+template <typename T, int EPI, int AL, bool KCHECK>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   constexpr int kEsz = (int)sizeof(T);
   constexpr int kBK = kTileBytes / kEsz;
-  constexpr bool kSwap = (EPI == EPI_STORE || EPI == EPI_DW);
+  constexpr bool kSwap = EPI == EPI_DW;
+  constexpr bool kAmn = AL != A_K;  // MN-contig LDS layout (MN-contig or blocked A)
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -885,19 +780,21 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
   const int kb = split * g.k_per_split;
   const int ke = min(g.K, kb + g.k_per_split);
 
-  Operand<T, A_MN> opa;
+  Operand<T, AL> opa;
   opa.init(g.A, g.lda, m0, min(kTile, g.M - m0), kb, ke, w, lane, wm * 128);
   const int khalf = lane >> 5;
   int swi[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) swi[i] = swz_k(i * 32 + (lane & 31));
 
-  // B: this wave's four column blocks start at jb0; K-pair q of this split is fragment q0 + q.
+  // B: this wave's four column blocks start at jb0 (the descriptor's base; blocks at or beyond
+  // NB read zeros); K-pair q of this split is fragment q0 + q of a block.
   const int KP = (int)g.ldb;
   const int NB = (g.N + 31) >> 5;
-  const __amdgpu_buffer_rsrc_t rb =
-      make_rsrc(g.B, __builtin_amdgcn_readfirstlane((uint32_t)NB * (uint32_t)KP * 1024u));
   const int jb0 = (n0 + wn * 128) >> 5;
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(
+      (const void*)uniform64((uint64_t)((const char*)g.B + (size_t)jb0 * KP * 1024)),
+      __builtin_amdgcn_readfirstlane((uint32_t)max(0, min(4, NB - jb0)) * (uint32_t)KP * 1024u));
   const uint32_t bvoff = (uint32_t)lane * 16u;
   const int q0 = kb * kEsz / 32;
   const int qend = ((ke - kb) * kEsz + 31) / 32;
@@ -909,7 +806,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     char* st = smem + (t & (kXbASlots - 1)) * kOperandBytes + w * 8 * 1024;
 #pragma unroll
     for (int j = 2 * pq; j < 2 * pq + 2; ++j) {
-      if constexpr (KCHECK && !A_MN) dma16(r, st + j * 1024, opa.offset(t, j));
+      if constexpr (KCHECK && AL == A_K) dma16(r, st + j * 1024, opa.offset(t, j));
       else dma16(r, st + j * 1024, opa.lane_offset(j), opa.uniform_offset(t, j));
     }
   };
@@ -924,7 +821,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
   auto load_b = [&](int q, auto slot) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t so = q < qend ? (uint32_t)((jb0 + j) * KP + q0 + q) * 1024u : kOOB;
+      const uint32_t so = q < qend ? (uint32_t)(j * KP + q0 + q) * 1024u : kOOB;
       vb[decltype(slot)::value][j] = __builtin_bit_cast(f32x4, load16(rb, bvoff, __builtin_amdgcn_readfirstlane(so)));
     }
   };
@@ -941,9 +838,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
 #pragma unroll
     for (int i = 0; i < 4; ++i) fa[buf][i] = opa.fragment(sa, p, i, khalf, swi[i]);
   };
-  // See gemm_kernel: transposing reads are invisible to the compiler's waits.
+  // Fragment reads issued as inline assembly are invisible to the compiler's wait insertion: at
+  // the start of each section wait for all earlier LDS traffic (the previous section's reads, long
+  // since done), with the fragment registers as operands so that no MFMA moves above the wait.
   auto sync_frags = [&]() {
-    if constexpr (A_MN && kEsz == 2) {
+    if constexpr (kAmn && kEsz == 2) {
       asm volatile("s_waitcnt lgkmcnt(0)"
                    : "+v"(fa[0][0]), "+v"(fa[0][1]), "+v"(fa[0][2]), "+v"(fa[0][3]), "+v"(fa[1][0]),
                      "+v"(fa[1][1]), "+v"(fa[1][2]), "+v"(fa[1][3])
@@ -960,7 +859,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
         else mfma_pair<T>(acc[i][j], fa[buf][i], vb[decltype(slot)::value][j]);
       }
   };
-  constexpr int kReads = A_MN ? 0 : 4;  // compiler-visible LDS reads per section
+  constexpr int kReads = kAmn ? 0 : 4;  // compiler-visible LDS reads per section
   // The section's LDS reads after its first MFMAs, its six loads after MFMAs 1, 3, .., 11.
   auto sched = []() {
     if constexpr (kEsz != 2) return;  // fp32: 64 MFMAs per section; left to the compiler
@@ -991,7 +890,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     // Loads retire in issue order, so a B load waits for every A load issued before it. With A
     // K-contiguous (W, streamed from HBM) the section issues its B fragments first (measured 4%
     // faster on the logits GEMM); with A MN-contiguous (dZ^T) the order made no difference.
-    if constexpr (!A_MN) {
+    if constexpr (!kAmn) {
       mma(s & 1, std::integral_constant<int, s>{});
       load_b(4 * kt + s + 7, std::integral_constant<int, (s + 7) & 7>{});
       load_a_q(ktp + kXbAhead, std::integral_constant<int, p>{});
@@ -1003,6 +902,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     sched();
   };
 
+  // 16-bit dW accumulation (chunks after the first): the tile's current dW values are loaded here,
+  // raw, in flight together with the loads that fill the pipeline, and become the accumulators'
+  // starting values, so the epilogue only stores. (fp32 adds them in the epilogue instead: its
+  // 256 values per lane would not fit next to the pipeline's registers.)
   const int mw = m0 + wm * 128, nw = n0 + wn * 128;
   constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
   const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;

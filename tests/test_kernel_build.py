@@ -18,13 +18,11 @@ from paper_2603_16428_amd import build as B
 
 # Element types: bf16 (DF16b), fp16 (DF16_), fp32 (f).
 TYPES = ("DF16b", "DF16_", "f")
-# gemm_kernel (both operands through LDS): the dH GEMM (epilogue 2, A K-contiguous, B MN-contiguous).
-LDS_GEMMS = [f"_ZN3lce11gemm_kernelI{t}Li2ELb0ELb1ELb0EEEvNS_8GemmArgsE" for t in TYPES]
-# gemm_xb_kernel (B from a blocked copy, straight to registers): (epilogue, A MN-contiguous, per-chunk
-# K check) of the logits GEMMs (forward / backward, with and without the K check) and dW.
-XB_VARIANTS = [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1), (3, 1, 0)]
-XB_GEMMS = [f"_ZN3lce14gemm_xb_kernelI{t}Li{e}ELb{a}ELb{c}EEEvNS_8GemmArgsE" for t in TYPES for e, a, c in XB_VARIANTS]
-GEMMS = LDS_GEMMS + XB_GEMMS
+# gemm_xb_kernel (B blocked, straight to registers): (epilogue, A layout 0 K-contiguous / 1 MN-
+# contiguous / 2 blocked, per-chunk K check) of the logits GEMMs (forward / backward, with and
+# without the K check), dH and dW.
+XB_VARIANTS = [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1), (2, 1, 0), (3, 2, 0)]
+GEMMS = [f"_ZN3lce14gemm_xb_kernelI{t}Li{e}ELi{a}ELb{c}EEEvNS_8GemmArgsE" for t in TYPES for e, a, c in XB_VARIANTS]
 
 
 @pytest.fixture(scope="module")
@@ -73,24 +71,18 @@ def test_gemm_main_loop_has_no_scratch_traffic(asm, name):
     vload = [l for l in loop if l.startswith("buffer_load") and not l.endswith("lds")]
     writes = [l for l in loop if l.startswith("ds_write")]
     tr = [l for l in loop if l.startswith("ds_read_b64_tr_b16")]
-    # Two K-tiles per loop trip: 2 x 64 MFMA steps (x4 for fp32's 32x32x2). gemm_kernel: 2 x 8 loads
-    # of each kind, B written to LDS. gemm_xb_kernel: A by LDS-DMA (2 x 8), B fragments straight to
-    # registers (2 x 16), nothing written to LDS.
+    # Two K-tiles per loop trip: 2 x 64 MFMA steps (x4 for fp32's 32x32x2); A by LDS-DMA (2 x 8), B
+    # fragments straight to registers (2 x 16), nothing written to LDS.
     assert len(mfma) == (128 if "DF16" in name else 512), len(mfma)
-    xb = name in XB_GEMMS
-    if xb:
-        assert len(dma) == 16 and len(vload) == 32 and len(writes) == 0, (len(dma), len(vload), len(writes))
-    else:
-        assert len(dma) == 16 and len(vload) == 16 and len(writes) == 16
-    # MN-contiguous 16-bit operands read from LDS: 2 transposing reads per fragment x 4 fragments per
-    # K-pair x 4 K-pairs per K-tile x 2 K-tiles.
-    flags = [int(f[0]) for f in name.split("ELb")[1:]]
-    n_mn = flags[0] if xb else flags[0] + flags[1]
-    assert len(tr) == (2 * 4 * 4 * 2 * n_mn if "DF16" in name else 0), len(tr)
+    assert len(dma) == 16 and len(vload) == 32 and len(writes) == 0, (len(dma), len(vload), len(writes))
+    # A in the MN-contiguous LDS layout (MN-contiguous or blocked), 16-bit: 2 transposing reads per
+    # fragment x 4 fragments per K-pair x 4 K-pairs per K-tile x 2 K-tiles.
+    layout = int(name.split("ELi")[1][0])
+    assert len(tr) == (2 * 4 * 4 * 2 if "DF16" in name and layout > 0 else 0), len(tr)
 
 
 # ---- LDS layout model: the index formulas of the GEMM loaders and fragment reads -------------
-# These restate, in Python, the per-lane formulas of gemm_kernel (Operand::init / offset /
+# These restate, in Python, the per-lane formulas of operand A's loader (Operand::init / offset /
 # fragment) and check that every fragment read finds the element the loader put there.
 
 def _swz_k(r):
@@ -252,3 +244,134 @@ def test_blocked_operand_layout_model(N, K, esz):
                 kbytes = 128 * t + 32 * p + 16 * h          # the A fragment's K bytes for this lane
                 want = [(32 * jb + (l & 31), kbytes // esz + e) for e in range(16 // esz)]
                 assert [g for g in got if g is not None] == [w for w in want if w[0] < N and w[1] < K]
+
+
+# ---- Blocked operand A (dZ of the dW GEMM) and the writers of e / dZ ----------------------------
+# Restated from Operand::init / rsrc (A_BLK), the LSE epilogue's blocked store and dlogits_kernel.
+
+def _blocked_decode(off, KP, esz):
+    # Byte offset into the blocked buffer -> (column = token, first K element = vocabulary id).
+    jb, rem = divmod(off, KP * 1024)
+    q, r = divmod(rem, 1024)
+    lf, b = divmod(r, 16)
+    assert b == 0
+    return 32 * jb + (lf & 31), (32 * q + 16 * (lf >> 5)) // esz
+
+
+@pytest.mark.parametrize("KP", [32, 16032])
+def test_blocked_a_fp32_loader_fetches_the_mn_loaders_pieces(KP):
+    # fp32 blocked A: relative to the K-tile's first token and the tile's first id, load j of wave
+    # w, lane l must fetch the piece (K-row, ids) that the MN-contiguous loader puts in the same
+    # LDS slot, inside the descriptor's range (the tile's ids in the K-tile's one token block).
+    esz = 4
+    for w in range(4):
+        for j in range(8):
+            for lane in range(64):
+                off = 8 * w * 16 + j * 16 + (lane << 9)
+                assert _blocked_decode(off, KP, esz) == (8 * w + j, 4 * lane)
+                assert off + 16 <= 256 * esz * 32
+
+
+@pytest.mark.parametrize("KP", [16, 8016])
+def test_blocked_a_16bit_loads_whole_fragments(KP):
+    # 16-bit blocked A: each load reads one whole fragment (1 KB, contiguous), slot 8w + j holds
+    # fragment (w/2, 8 (w%2) + j), and with one token block left in the K-tile the descriptor's
+    # range (the tile's ids in that block) takes exactly the first block's loads.
+    esz, tile_bytes = 2, 256 * 2 * 32
+    for w in range(4):
+        for j in range(8):
+            offs = []
+            for lane in range(64):
+                slot_x = (lane ^ (4 * (lane >> 5))) << 4
+                offs.append((w >> 1) * KP * 1024 + (w & 1) * 8192 + j * 1024 + (slot_x ^ (128 if j & 1 else 0)))
+            base = (w >> 1) * KP * 1024 + (8 * (w & 1) + j) * 1024
+            assert sorted(offs) == list(range(base, base + 1024, 16))
+            assert all((o + 16 <= tile_bytes) == (w < 2) for o in offs)
+
+
+@pytest.mark.parametrize("esz", [2, 4])
+def test_lse_epilogue_stores_e_blocked(esz):
+    # The LSE_BWD epilogue: for block (i, j) of the wave at (mw, nw), lane l's token is column
+    # nw + 32 j + l%32 and its piece of each fragment of that token block is at l * 16.
+    KP = 64 if esz == 2 else 128
+    for mw, nw in ((0, 0), (128, 128), (768, 224)):
+        for j in range(4):
+            for i in range(4):
+                for lane in range(64):
+                    h = lane >> 5
+                    tok = nw + 32 * j + (lane & 31)
+                    e_blk = ((nw + 32 * j) >> 5) * KP * 1024 + lane * 16
+                    if esz == 2:
+                        # after regroup32: ids 8h .. and 16 + 8h .. of the 32-id segment
+                        lo = e_blk + ((mw + 32 * i) >> 4) * 1024
+                        assert _blocked_decode(lo, KP, esz) == (tok, mw + 32 * i + 8 * h)
+                        assert _blocked_decode(lo + 1024, KP, esz) == (tok, mw + 32 * i + 16 + 8 * h)
+                    else:
+                        for q in range(4):
+                            off = e_blk + ((mw + 32 * i + 8 * q) >> 3) * 1024
+                            assert _blocked_decode(off, KP, esz) == (tok, mw + 32 * i + 8 * q + 4 * h)
+
+
+@pytest.mark.parametrize("esz", [2, 4])
+def test_dlogits_pieces(esz):
+    # dlogits_kernel: block (b, jb), wave w, lane l, piece k -- its token and ids, and the claim
+    # that the four pieces of a lane lie in one 128-id slice; the grid writes every piece once.
+    KP, NB = 32 if esz == 2 else 64, 3
+    seen = set()
+    for jb in range(NB):
+        for b in range(KP // 16):
+            for w in range(4):
+                for lane in range(64):
+                    q0 = 16 * b + 4 * w
+                    v0 = (q0 * 32 + 16 * (lane >> 5)) // esz
+                    slices = set()
+                    for k in range(4):
+                        off = (jb * KP + q0) * 1024 + lane * 16 + k * 1024
+                        v = v0 + k * (32 // esz)
+                        assert _blocked_decode(off, KP, esz) == (32 * jb + (lane & 31), v)
+                        slices |= {(v + e) // 128 for e in range(16 // esz)}
+                        seen.add(off)
+                    assert len(slices) == 1 and slices == {v0 // 128}
+    assert seen == set(range(0, NB * KP * 1024, 16))
+
+
+def test_blocked_a_16bit_lds_layout_model():
+    # 16-bit blocked A: whole-fragment loads with a piece permutation, and the transposing fragment
+    # reads (as in test_mn_contiguous_bf16_layout_model): every lane must receive the four tokens
+    # of its id that the MFMA expects, with no LDS bank conflicts.
+    KP, esz = 64, 2
+    stored = {}   # LDS byte -> (token, id) of its first bf16, relative to the K-tile and the tile
+    for w in range(4):
+        for j in range(8):
+            row_off = (w >> 1) * KP * 1024 + (w & 1) * 8192
+            for lane in range(64):
+                slot_x = (lane ^ (4 * (lane >> 5))) << 4
+                off = row_off + j * 1024 + (slot_x ^ (128 if j & 1 else 0))
+                tok, idx = _blocked_decode(off, KP, esz)
+                lds = (8 * w + j) * 1024 + lane * 16
+                for e in range(8):
+                    stored[lds + 2 * e] = (tok, idx + e)
+    assert len(stored) == 32 * 1024 // 2
+    conflicts = 0
+    for wsub in (0, 128):
+        for i in range(4):
+            for p in range(4):
+                for s in range(2):
+                    got, addrs = {}, []
+                    for lane in range(64):
+                        g, ip = lane >> 4, lane & 15
+                        h = (ip & 3) >> 1
+                        frag0 = (wsub // 16 + (g & 1)) * 1024 + 16 * ((ip >> 2) + 4 * h + 8 * ((g >> 1) ^ (g & 1)) + 32 * h) + 8 * (ip & 1)
+                        a = ((frag0) ^ (64 * s)) + 16384 * (p >> 1) + 256 * (p & 1) + 2048 * i
+                        addrs.append(a)
+                        got[lane] = [stored[a + 2 * e] for e in range(4)]   # 4 consecutive ids of a token
+                    for lane in range(64):   # the transposed delivery of ds_read_b64_tr_b16
+                        g, jj = lane >> 4, lane & 15
+                        recv = [got[16 * g + 4 * e + jj // 4][jj % 4] for e in range(4)]
+                        k0 = 16 * p + 8 * (lane >> 5) + 4 * s
+                        assert recv == [(k0 + e, wsub + 32 * i + (lane & 31)) for e in range(4)]
+                    for nb, grp in ((32, 16), (64, 32)):
+                        for g0 in range(0, 64, grp):
+                            banks = [((a // 4) + b) % nb for a in addrs[g0:g0 + grp] for b in (0, 1)]
+                            conflicts += len(banks) - len(set(banks))
+    assert conflicts == 0
