@@ -39,8 +39,11 @@
  *   - A non-ignored label outside [0, V) is not an error the call can report (labels live on the
  *     device); its token's loss becomes NaN and it contributes no one-hot term to the gradients.
  *   - MEAN with no valid token gives loss 0 and zero gradients.
- *   - Supported shapes: N, H, V >= 1; H a multiple of 8 (BF16, FP16) or 4 (FP32); V * H and N * H
- *     below 2^31 elements per 256-row slice limits (see LCE_ERR_UNSUPPORTED).
+ *   - Supported shapes: N, H, V >= 1 and below 2^30; H a multiple of 8 (BF16, FP16) or 4 (FP32);
+ *     256 x max(H, V rounded up to 256) elements below 2^31 bytes; a chunk's blocked copies of X
+ *     below 2^31 bytes and a chunk of at most 2,097,088 tokens (65534 blocks of 32); with the
+ *     RMSNorm backward, N at most 4,194,240 (65535 blocks of 64 rows). Other sizes give
+ *     LCE_ERR_UNSUPPORTED.
  */
 #ifndef LCE_H_
 #define LCE_H_

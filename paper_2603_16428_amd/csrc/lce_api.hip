@@ -147,6 +147,8 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   if (p.xk_nb * p.xk_kp * 1024 > lim || p.xm_nb * p.xm_kp * 1024 > lim) return LCE_ERR_UNSUPPORTED;
   p.ez_nb = p.ncp / 32;
   p.ez_kp = round_up(V, kTile) * p.esz / 32;
+  // Grid y dimensions (at most 65535): dlogits_kernel's token blocks, block_mn_kernel's K-pair groups.
+  if (p.ez_nb > 65535 || cdiv(p.xm_kp, 4) > 65535) return LCE_ERR_UNSUPPORTED;
 
   if (backward) {
     // dH tiles of one chunk: split the vocabulary (K) so that the grid fills the device.
@@ -397,6 +399,7 @@ lce_status_t make_rms_plan(int64_t N, int64_t H, int64_t V, int dtype, bool back
   rp.o_r = take((size_t)N * 4);
   if (backward) {
     rp.row_blocks = cdiv(N, kRmsRows);
+    if (rp.row_blocks > 65535) return LCE_ERR_UNSUPPORTED;  // rmsnorm_backward_kernel's grid y
     rp.o_dx = take((size_t)N * H * 4);
     rp.o_s = take((size_t)N * 4);
     rp.o_part = take((size_t)rp.row_blocks * H * 4);

@@ -61,6 +61,9 @@ def test_workspace_size(lib):
     assert ws(8, 12, 8, FP32, 1, 0) > 0           # fine for fp32
     assert ws(8, 16, 8, FP16, 1, 0) == ws(8, 16, 8, BF16, 1, 0) > 0  # same 2-byte layout
     assert ws(300, 64, 100, BF16, 1, 100) == 0    # chunk must be a multiple of 64 when < N
+    # chunks of more than 65535 token blocks of 32 would exceed a grid's y dimension
+    assert ws(32767 * 64, 64, 256, BF16, 1, 32767 * 64) > 0
+    assert ws(32768 * 64, 64, 256, BF16, 1, 32768 * 64) == 0
     fwd = ws(8192, 4096, 128256, BF16, 0, 0)
     bwd = ws(8192, 4096, 128256, BF16, 1, 0)
     assert 0 < fwd < bwd
@@ -118,6 +121,9 @@ def test_rmsnorm_workspace_size(lib):
     ws = lib.lce_rmsnorm_workspace_size
     assert ws(0, 8, 8, BF16, 1, 0) == 0
     assert ws(8, 12, 8, BF16, 1, 0) == 0           # same shape rules as the plain step
+    assert ws(65535 * 64, 8, 8, BF16, 1, 64) > 0   # rows of 64 per backward block: grid y <= 65535
+    assert ws(65535 * 64 + 1, 8, 8, BF16, 1, 64) == 0
+    assert ws(65535 * 64 + 1, 8, 8, BF16, 0, 64) > 0
     base = lib.lce_workspace_size(8192, 4096, 128256, BF16, 1, 0)
     extra = ws(8192, 4096, 128256, BF16, 1, 0) - base
     # x [N,H] bf16, dX [N,H] fp32, one chunk's fp32 dH partials (4096 x 4096 here), r and s [N],
