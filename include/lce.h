@@ -71,10 +71,13 @@ typedef enum { LCE_REDUCTION_NONE = 0, LCE_REDUCTION_MEAN = 1, LCE_REDUCTION_SUM
 /*
  * Bytes of device workspace needed by lce_forward (with_backward = 0) or lce_forward_backward
  * (with_backward = 1) for these sizes. chunk_tokens is the number of tokens processed per chunk
- * (0 = automatic: the largest multiple of 64 not above min(H, ceil(N/2)), at least 64; a nonzero
- * value smaller than N must be a multiple of 64). The workspace holds O(chunk_tokens * (V + H) + N)
- * elements (one chunk's logits-shaped buffer, two rearranged copies of the chunk's hidden rows,
- * per-token vectors); the N x V logits never exist. Returns 0 for invalid arguments.
+ * (0 = automatic: with backward, the largest multiple of 64 not above min(H, ceil(N/2)), at least
+ * 64; forward only, all N tokens up to 16384, else chunks of 16384 or the backward size if larger;
+ * a nonzero value smaller than N must be a multiple of 64). The workspace holds
+ * O(chunk_tokens * (V + H) + N) elements with backward (one chunk's logits-shaped buffer, two
+ * rearranged copies of the chunk's hidden rows, per-token vectors) and O(chunk_tokens * (V / 64 +
+ * H) + N) forward only (per-slice partials instead); the N x V logits never exist. Returns 0 for
+ * invalid arguments.
  */
 size_t lce_workspace_size(int64_t N, int64_t H, int64_t V, int dtype, int with_backward,
                           int64_t chunk_tokens);

@@ -109,6 +109,8 @@ int num_cus() {
   return c;
 }
 
+constexpr int64_t kFwdChunk = 16384;  // automatic forward chunk (a multiple of 64)
+
 int64_t auto_chunk(int64_t N, int64_t H) {
   const int64_t half = cdiv(N, 2);
   int64_t nc = std::min(H, half) / 64 * 64;
@@ -127,7 +129,13 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.esz = dtype == LCE_DTYPE_FP32 ? 4 : 2;
   p.backward = backward;
   if (H % (16 / p.esz) != 0) return LCE_ERR_UNSUPPORTED;
-  int64_t nc = chunk_tokens == 0 ? auto_chunk(N, H) : chunk_tokens;
+  // Automatic chunks: a training step keeps one chunk's e/dZ, so its chunks stay small; a forward
+  // call keeps only per-slice partials (N V / 16 bytes), so it takes up to 16384 tokens at once
+  // (one launch of the logits GEMM instead of several, each with a partly empty last wave).
+  int64_t nc = chunk_tokens != 0 ? chunk_tokens
+               : backward      ? auto_chunk(N, H)
+               : N <= kFwdChunk ? N
+                                : std::max(auto_chunk(N, H), kFwdChunk);
   if (nc >= N) nc = N;
   else if (nc % 64 != 0) return LCE_ERR_INVALID_ARGUMENT;
   p.nc = nc;

@@ -76,6 +76,11 @@ def test_workspace_size(lib):
     assert lib.lce_auto_chunk_tokens(16384, 3584, 152064, BF16) == 3584
     assert lib.lce_auto_chunk_tokens(4096, 12288, 32768, BF16) == 2048
     assert lib.lce_auto_chunk_tokens(37, 72, 1000, BF16) == 37  # one chunk
+    # Forward only: one chunk up to 16384 tokens (per-slice partials, no logits-shaped buffer).
+    one = ws(8192, 4096, 128256, BF16, 0, 8192)
+    assert fwd == one
+    assert ws(8192, 4096, 128256, BF16, 0, 4096) < one < bwd / 4
+    assert ws(40000, 4096, 128256, BF16, 0, 0) == ws(40000, 4096, 128256, BF16, 0, 16384)
 
 
 def _fwd(lib, **kw):
