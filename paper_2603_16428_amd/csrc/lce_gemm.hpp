@@ -485,45 +485,62 @@ struct Operand {
   }
 };
 
-// 16-bit dW accumulation (chunks after the first): the wave's current dW values in the swapped
-// accumulator layout, loaded raw while the pipeline fills, then the accumulators' starting values.
-// They enter divided by the factor the epilogue will apply (the dz storage scale, 1 for bf16), so
-// that the epilogue's one multiply gives dW + factor * (this chunk's sum); a zero factor (a mean
-// over no valid token) starts them at zero.
+// 16-bit dW accumulation (chunks after the first): the wave's current dW values, loaded raw while
+// the pipeline fills, then the accumulators' starting values. Each lane loads the two 16-byte row
+// pieces that store_row32 writes from it (lanes l and l + 32 cover 32 contiguous bytes of a row per
+// load), and one v_permlane32_swap per dword -- the inverse of regroup32's, which is its own
+// inverse -- returns the elements to the swapped accumulator layout. They enter divided by the
+// factor the epilogue will apply (the dz storage scale, 1 for bf16), so that the epilogue's one
+// multiply gives dW + factor * (this chunk's sum); a zero factor (a mean over no valid token)
+// starts them at zero.
 template <typename T>
-using vec4_t = T __attribute__((ext_vector_type(4)));
-
-template <typename T>
-__device__ __forceinline__ void load_dw_prev(const GemmArgs& g, vec4_t<T> (&prev)[4][4][4], int mw, int nw, int lane) {
-  typedef vec4_t<T> t4;
-  const int sub4 = 4 * (lane >> 5);
+__device__ __forceinline__ void load_dw_prev(const GemmArgs& g, u32x4 (&prev)[4][4][2], int mw, int nw, int lane) {
+  const int half = lane >> 5;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = mw + 32 * i + (lane & 31);
     const T* o = (const T*)g.out + (size_t)row * g.ldo;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = nw + 32 * j + 8 * q + sub4;
-        prev[i][j][q] = (row < g.M && col < g.N) ? *(const t4*)(o + col) : (t4){};
-      }
+    for (int j = 0; j < 4; ++j) {
+      // N (the output pitch) is a multiple of 8: a 16-byte piece is all in or all out.
+      const int c0 = nw + 32 * j + 8 * half;
+      prev[i][j][0] = (row < g.M && c0 < g.N) ? *(const u32x4*)(o + c0) : (u32x4){};
+      prev[i][j][1] = (row < g.M && c0 + 16 < g.N) ? *(const u32x4*)(o + c0 + 16) : (u32x4){};
+    }
   }
 }
 
 template <typename T>
-__device__ __forceinline__ void apply_dw_prev(f32x16 (&acc)[4][4], const vec4_t<T> (&prev)[4][4][4], float inv_scale) {
+__device__ __forceinline__ void apply_dw_prev(f32x16 (&acc)[4][4], const u32x4 (&prev)[4][4][2], float inv_scale) {
+  typedef T t4 __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) {
+      const u32x4 lo = prev[i][j][0], hi = prev[i][j][1];
+      // regroup32 left lo = (a0, a1, b0, b1), hi = (a2, a3, b2, b3) after its swap.
+      uint32_t a[4] = {lo[0], lo[1], hi[0], hi[1]};
+      uint32_t b[4] = {lo[2], lo[3], hi[2], hi[3]};
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int e = 0; e < 4; ++e) {
+        const auto r = __builtin_amdgcn_permlane32_swap(a[e], b[e], false, false);
+        a[e] = r[0];
+        b[e] = r[1];
+      }
+      // Now a = (q0, q2), b = (q1, q3): the lane's 4-element groups at 8q + 4 (l / 32).
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t* d = (q & 1) ? b : a;
+        const t4 x = __builtin_bit_cast(t4, (u32x2){d[(q >> 1) * 2], d[(q >> 1) * 2 + 1]});
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float x = (float)prev[i][j][q][e];
-          acc[i][j][4 * q + e] = Storage<T>::kDzUnscaled ? x * inv_scale : x;
+          const float v = (float)x[e];
+          acc[i][j][4 * q + e] = Storage<T>::kDzUnscaled ? v * inv_scale : v;
         }
+      }
+      // One block at a time: interleaved, the conversions' temporaries outgrow the registers.
+      __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
 // The epilogue factor's reciprocal for apply_dw_prev (0 when the factor is 0).
@@ -909,7 +926,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
   const int mw = m0 + wm * 128, nw = n0 + wn * 128;
   constexpr bool kPreload = EPI == EPI_DW && kEsz == 2;
   const bool accumulate = EPI == EPI_DW && g.mode == DW_ACCUMULATE;
-  vec4_t<T> prev[kPreload ? 4 : 1][4][4];
+  u32x4 prev[kPreload ? 4 : 1][4][2];
   if constexpr (kPreload) {
     if (accumulate) load_dw_prev<T>(g, prev, mw, nw, lane);
   }
@@ -919,14 +936,18 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     // Prologue: A(0 .. ahead-1), then B(0 .. 6). A(0) has landed for every wave (issued after it:
     // the other A K-tiles and 28 B loads) before its first fragments are read; the first waits at
     // p == 3 find at least as many loads after A(1), A(2) as they allow. The dW values (128 VGPRs
-    // raw) become accumulators once the first three K-pairs of B are on their way, before the rest
-    // of B's ring fills the registers.
+    // raw) become accumulators before the rest of B's ring fills the registers: bf16's once the
+    // first three K-pairs of B are on their way, fp16's before any.
 #pragma unroll
     for (int t = 0; t < kXbAhead; ++t) load_a(t);
+    // fp16's values are also scaled as they enter: its temporaries fit only before B's ring fills.
+    if constexpr (kPreload && Storage<T>::kDzUnscaled) {
+      if (accumulate) apply_dw_prev<T>(acc, prev, dw_prev_scale<T>(g));
+    }
     load_b(0, std::integral_constant<int, 0>{});
     load_b(1, std::integral_constant<int, 1>{});
     load_b(2, std::integral_constant<int, 2>{});
-    if constexpr (kPreload) {
+    if constexpr (kPreload && !Storage<T>::kDzUnscaled) {
       if (accumulate) apply_dw_prev<T>(acc, prev, dw_prev_scale<T>(g));
     }
     load_b(3, std::integral_constant<int, 3>{});
