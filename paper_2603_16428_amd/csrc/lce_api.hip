@@ -76,6 +76,11 @@ struct Plan {
   int64_t N = 0, H = 0, V = 0;
   int esz = 0;
   bool backward = false;
+  // Backward with target-referenced e (bf16, fp32): the logits epilogue stores exp(z - z_target),
+  // combine folds the one-hot term into e and leaves a per-token factor for the dH epilogue and
+  // the dW operand, and no dlogits pass runs unless a chunk's flag asks for the slice-maximum
+  // path. fp16 (whose exponent range cannot hold exp(z - z_target)) keeps the dlogits pass.
+  bool tref = false;
   int64_t nc = 0, chunks = 0;     // tokens per chunk, number of chunks
   int64_t ncp = 0;                // tokens per chunk rounded up to 64
   int64_t slices = 0;
@@ -89,6 +94,7 @@ struct Plan {
   int64_t ez_nb = 0, ez_kp = 0;
   // workspace offsets (bytes)
   size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_dhp = 0;
+  size_t o_scale = 0, o_flags = 0, o_ref = 0;
   size_t o_xk = 0, o_xm = 0;
   size_t total = 0;
 };
@@ -128,6 +134,7 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.N = N; p.H = H; p.V = V;
   p.esz = dtype == LCE_DTYPE_FP32 ? 4 : 2;
   p.backward = backward;
+  p.tref = backward && dtype != LCE_DTYPE_FP16;
   if (H % (16 / p.esz) != 0) return LCE_ERR_UNSUPPORTED;
   // Automatic chunks: a training step keeps one chunk's e/dZ, so its chunks stay small; a forward
   // call keeps only per-slice partials (N V / 16 bytes), so it takes up to 16384 tokens at once
@@ -155,7 +162,8 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   if (p.xk_nb * p.xk_kp * 1024 > lim || p.xm_nb * p.xm_kp * 1024 > lim) return LCE_ERR_UNSUPPORTED;
   p.ez_nb = p.ncp / 32;
   p.ez_kp = round_up(V, kTile) * p.esz / 32;
-  // Grid y dimensions (at most 65535): dlogits_kernel's token blocks, block_mn_kernel's K-pair groups.
+  // Grid y dimensions (at most 65535): block_mn_kernel's K-pair groups; a chunk's token blocks are
+  // held to the same bound.
   if (p.ez_nb > 65535 || cdiv(p.xm_kp, 4) > 65535) return LCE_ERR_UNSUPPORTED;
 
   if (backward) {
@@ -192,6 +200,9 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   if (backward) {
     p.o_xm = take((size_t)(p.xm_nb * p.xm_kp * 1024));
     p.o_e = take((size_t)(p.ez_nb * p.ez_kp * 1024));
+    p.o_scale = take((size_t)N * 4);
+    p.o_ref = take((size_t)N * 4);  // used by target-referenced plans (kept for all: one layout per element size)
+    p.o_flags = take((size_t)p.chunks * 4);
     if (p.dh_splits > 1 || dx_f32) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
   }
   p.total = off;
@@ -249,13 +260,17 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
   T* xk = (T*)(ws + p.o_xk);
   T* xm = p.backward ? (T*)(ws + p.o_xm) : nullptr;
   float* dhp = (p.backward && (p.dh_splits > 1 || dx32)) ? (float*)(ws + p.o_dhp) : nullptr;
+  float* scale = p.backward ? (float*)(ws + p.o_scale) : nullptr;
+  float* tref = p.tref ? (float*)(ws + p.o_ref) : nullptr;
+  int* flags = p.backward ? (int*)(ws + p.o_flags) : nullptr;
   const int mean = reduction == LCE_REDUCTION_MEAN;
 
   {
     KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(1024), 0, s, y, N, ignore_index, nvalid);
+    hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(1024), 0, s, y, N, ignore_index, nvalid, flags,
+                       (int64_t)(flags ? p.chunks : 0));
     hipLaunchKernelGGL((target_logit_kernel<T>), dim3((unsigned)cdiv(N, 4)), dim3(256), 0, s, X, W, y, N, H, V,
-                       ignore_index, tgt);
+                       ignore_index, tgt, tref);
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return LCE_ERR_HIP;
 
@@ -263,15 +278,19 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     const int64_t t0 = c * p.nc;
     const int rows = (int)std::min(p.nc, N - t0);
 
-    // Fragment-blocked copies of X_c: operand B of the logits GEMM and, backward, of the dW GEMM.
+    // Fragment-blocked copies of X_c: operand B of the logits GEMM and, backward, of the dW GEMM
+    // (target-referenced: scaled per token, so made once the factors are known).
+    auto block_x_for_dw = [&](const float* row_scale) {
+      KernelTimer t(T_OTHER, s);
+      hipLaunchKernelGGL((block_mn_kernel<T>), dim3((unsigned)p.xm_nb, (unsigned)cdiv(p.xm_kp, 4)), dim3(256), 0, s,
+                         X + t0 * H, H, (int)H, rows, (int)p.xm_kp, xm, row_scale);
+    };
     {
     KernelTimer t(T_OTHER, s);
     hipLaunchKernelGGL((block_k_kernel<T>), dim3((unsigned)cdiv(p.xk_nb * p.xk_kp * 64, 256)), dim3(256), 0, s,
                        X + t0 * H, H, rows, (int)H, (int)p.xk_kp, (int)p.xk_nb, xk);
-    if (p.backward)
-      hipLaunchKernelGGL((block_mn_kernel<T>), dim3((unsigned)p.xm_nb, (unsigned)cdiv(p.xm_kp, 4)), dim3(256), 0, s,
-                         X + t0 * H, H, (int)H, rows, (int)p.xm_kp, xm);
     }
+    if (p.backward && !p.tref) block_x_for_dw(nullptr);
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
 
     // logits^T tile = W . X_c^T with the log-sum-exp epilogue.
@@ -289,6 +308,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     const bool whole = H % (kTileBytes / p.esz) == 0;
     if (p.backward) {
       g.out = ez; g.ldo = p.ez_kp;
+      if (p.tref) g.ref = tref + t0;
       e = whole ? launch_gemm<T, EPI_LSE_BWD, A_K, false>(g, s) : launch_gemm<T, EPI_LSE_BWD, A_K, true>(g, s);
     } else {
       e = whole ? launch_gemm<T, EPI_LSE_FWD, A_K, false>(g, s) : launch_gemm<T, EPI_LSE_FWD, A_K, true>(g, s);
@@ -296,21 +316,43 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     }
     if (e != hipSuccess) return LCE_ERR_HIP;
 
-    {
-    KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)cdiv(rows, kCombineTokens)), dim3(256), 0, s, pmax, psum, p.ncp,
-                       (int)p.slices, rows, y + t0, ignore_index, tgt + t0, lse + t0, tl + t0);
-    }
+    auto combine = [&](int mode, const int* run_if) {
+      KernelTimer t(T_OTHER, s);
+      hipLaunchKernelGGL((combine_kernel<T>), dim3((unsigned)cdiv(rows, kCombineTokens)), dim3(256), 0, s, pmax, psum,
+                         p.ncp, (int)p.slices, rows, y + t0, ignore_index, tgt + t0, lse + t0, tl + t0, mode,
+                         scale ? scale + t0 : nullptr, (const int*)nvalid, mean, ez, p.ez_kp, V,
+                         flags ? flags + c : nullptr, run_if);
+    };
+    // dlogits, in place (blocked): a block per (K-pair group, token block), or a looped grid.
+    auto dlogits = [&](const int* run_if, int64_t grid) {
+      KernelTimer t(run_if ? T_OTHER : T_DLOGITS, s);
+      hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)grid), dim3(256), 0, s, ez, p.ez_kp, p.ez_nb, pmax, p.ncp,
+                         lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V, run_if);
+    };
+    combine(p.tref ? CMB_TREF : CMB_FORWARD, nullptr);
     if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
     if (!p.backward) continue;
 
-    // dlogits, in place (blocked).
-    {
-    KernelTimer t(T_DLOGITS, s);
-    hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)(p.ez_kp / 16), (unsigned)p.ez_nb), dim3(256), 0, s,
-                       ez, p.ez_kp, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V);
-    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
+    if (p.tref) {
+      // Only when combine flagged a token whose exp(z - z_target) may have overflowed: the chunk's
+      // logits again with slice-maximum references, combine, and dlogits (launches that return at
+      // once when the flag is clear).
+      const int* flag = flags + c;
+      GemmArgs gf = g;
+      gf.ref = nullptr; gf.run_if = flag;
+      {
+      KernelTimer t(T_OTHER, s);
+      const bool whole = H % (kTileBytes / p.esz) == 0;
+      e = whole ? launch_gemm<T, EPI_LSE_BWD, A_K, false>(gf, s) : launch_gemm<T, EPI_LSE_BWD, A_K, true>(gf, s);
+      }
+      if (e != hipSuccess) return LCE_ERR_HIP;
+      combine(CMB_SLICE, flag);
+      dlogits(flag, std::min<int64_t>(p.ez_kp / 16 * p.ez_nb, 4 * (int64_t)num_cus()));
+      block_x_for_dw(scale + t0);
+    } else {
+      dlogits(nullptr, p.ez_kp / 16 * p.ez_nb);
     }
+    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
 
     // dH rows of the chunk, as dH_c^T = W^T . dZ_c^T (A = W [V, H] MN-contig over H, B = dZ_c
     // blocked over the chunk's tokens), stored token-major.
@@ -326,6 +368,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
       gh.out = dH + t0 * H; gh.ldo = H; gh.mode = 0;
     }
     gh.n_valid = nvalid; gh.mean = mean;
+    if (p.tref) gh.col_scale = scale + t0;
     {
     KernelTimer t(T_DH, s);
     if (launch_gemm<T, EPI_STORE, A_MN>(gh, s) != hipSuccess) return LCE_ERR_HIP;

@@ -16,10 +16,13 @@ template <> __device__ __forceinline__ f16 from_f32<f16>(float v) { return (f16)
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
 // n_valid = number of labels different from ignore_index, over all N tokens (the mean's divisor
-// is global, never per chunk). One block of 1024 threads; fixed-order tree, so deterministic.
+// is global, never per chunk). One block of 1024 threads; fixed-order tree, so deterministic. Also
+// clears the chunks' fallback flags (see combine_kernel).
 __global__ __launch_bounds__(1024) void count_valid_kernel(const int64_t* __restrict__ y, int64_t N,
-                                                           int64_t ignore_index, int* __restrict__ n_valid) {
+                                                           int64_t ignore_index, int* __restrict__ n_valid,
+                                                           int* __restrict__ flags, int64_t nflags) {
   __shared__ int part[1024];
+  for (int64_t k = threadIdx.x; k < nflags; k += 1024) flags[k] = 0;
   int c = 0;
   for (int64_t i = threadIdx.x; i < N; i += 1024) c += (y[i] != ignore_index);
   part[threadIdx.x] = c;
@@ -32,21 +35,23 @@ __global__ __launch_bounds__(1024) void count_valid_kernel(const int64_t* __rest
 }
 
 // Target logit z_{i, y_i} = x_i . w_{y_i} in fp32, one wave per token. Ignored tokens get 0;
-// a label outside [0, V) gets NaN (so that the token's loss is NaN) and reads nothing.
+// a label outside [0, V) gets NaN (so that the token's loss is NaN) and reads nothing. ref
+// (optional): the reference of the target-referenced logits epilogue, z_{i, y_i} for a valid label
+// and NaN otherwise.
 template <typename T>
 __global__ __launch_bounds__(256) void target_logit_kernel(const T* __restrict__ X, const T* __restrict__ W,
                                                            const int64_t* __restrict__ y, int64_t N, int64_t H,
-                                                           int64_t V, int64_t ignore_index, float* __restrict__ tgt) {
+                                                           int64_t V, int64_t ignore_index, float* __restrict__ tgt,
+                                                           float* __restrict__ ref) {
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (i >= N) return;
   const int64_t lab = y[i];
-  if (lab == ignore_index) {
-    if (lane == 0) tgt[i] = 0.f;
-    return;
-  }
-  if (lab < 0 || lab >= V) {
-    if (lane == 0) tgt[i] = __builtin_nanf("");
+  if (lab == ignore_index || lab < 0 || lab >= V) {
+    if (lane == 0) {
+      tgt[i] = lab == ignore_index ? 0.f : __builtin_nanf("");
+      if (ref != nullptr) ref[i] = __builtin_nanf("");
+    }
     return;
   }
   constexpr int kVec = 16 / sizeof(T);
@@ -59,20 +64,42 @@ __global__ __launch_bounds__(256) void target_logit_kernel(const T* __restrict__
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-  if (lane == 0) tgt[i] = s;
+  if (lane == 0) {
+    tgt[i] = s;
+    if (ref != nullptr) ref[i] = s;
+  }
 }
 
 // Row combine. For each token of the chunk: M = max_t m_t, lse = M + log sum_t s_t exp(m_t - M),
 // and the token loss lse - z_target (0 for ignored tokens). A block takes 16 tokens x 16 slice
 // groups: thread (token j, group k) merges slices k, k + 16, ... in increasing order (a 64-byte
 // coalesced row of partials per slice), then group 0 merges the 16 groups in a fixed order.
+//
+// Backward, the per-token factor that the dH epilogue and the dW operand apply (scale_out):
+//   CMB_TREF  : e holds exp(z - z_target) for valid tokens (label in [0, V), not ignored), and the
+//               partials were taken relative to z_target, so S = sum_v exp(z_v - z_target) =
+//               exp(lse - z_target) is the merged sum. dZ = g (p - onehot) = (g / S) (e - S onehot):
+//               the factor is g / S (0 for other tokens) and the label's entry of e becomes e - S.
+//               A token whose S exceeds kTrefMaxSum (loss above 60), or is not finite or below the
+//               target's own term 1 (inputs that are not finite), sets *flag: its e may have
+//               overflowed, so the chunk is redone with slice-maximum references.
+//   CMB_SLICE : dlogits forms dZ with g inside; the factor is 1.
+// run_if: do nothing unless *run_if != 0 (nullptr: always run).
+enum CombineMode { CMB_FORWARD = 0, CMB_TREF = 1, CMB_SLICE = 2 };
+constexpr float kTrefMaxSum = 1.1420073898e26f;  // exp(60)
 constexpr int kCombineTokens = 16;
+template <typename T>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ pmax, const float* __restrict__ psum,
                                                       int64_t ldp, int slices, int rows,
                                                       const int64_t* __restrict__ y, int64_t ignore_index,
                                                       const float* __restrict__ tgt,
                                                       float* __restrict__ lse_out,     // [rows] (chunk-offset)
-                                                      float* __restrict__ loss_out) {  // [rows] (chunk-offset)
+                                                      float* __restrict__ loss_out,    // [rows] (chunk-offset)
+                                                      int mode, float* __restrict__ scale_out,
+                                                      const int* __restrict__ n_valid, int mean, T* __restrict__ ez,
+                                                      int64_t KP, int64_t V, int* __restrict__ flag,
+                                                      const int* __restrict__ run_if) {
+  if (run_if != nullptr && *run_if == 0) return;
   __shared__ float sm[16][kCombineTokens], ss[16][kCombineTokens];
   const int t = threadIdx.x % kCombineTokens, grp = threadIdx.x / kCombineTokens;
   const int i = blockIdx.x * kCombineTokens + t;
@@ -94,8 +121,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     float S = 0.f;
     for (int k = 0; k < 16; ++k) S += ss[k][t] * __expf(sm[k][t] - M);
     const float lse = M + __logf(S);
+    const int64_t lab = y[i];
     lse_out[i] = lse;
-    loss_out[i] = (y[i] == ignore_index) ? 0.f : lse - tgt[i];
+    loss_out[i] = (lab == ignore_index) ? 0.f : lse - tgt[i];
+    if (mode == CMB_TREF) {
+      float sc = 0.f;
+      if (lab != ignore_index && lab >= 0 && lab < V) {
+        const float sum = S * __expf(M - tgt[i]);  // every m_t is tgt[i] here, so this is S
+        if (sum >= 1.f && sum <= kTrefMaxSum) {  // (the target's own term is 1; NaN fails too)
+          const int nv = *n_valid;
+          const float g = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
+          sc = g / sum;
+          // Element (token i, id lab) of the blocked layout.
+          const int64_t byte = lab * (int64_t)sizeof(T);
+          const int ln = (i & 31) + 32 * (int)((byte >> 4) & 1);
+          T* p = (T*)((char*)ez + ((size_t)(i >> 5) * KP + (size_t)(byte >> 5)) * 1024 + ln * 16 + (byte & 15));
+          *p = from_f32<T>(to_f32(*p) - sum);
+        } else {
+          *flag = 1;
+        }
+      }
+      scale_out[i] = sc;
+    } else if (mode == CMB_SLICE) {
+      scale_out[i] = 1.f;
+    }
   }
 }
 
@@ -111,15 +160,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 // slice, so each lane has one token and one scale. For fp16 both e and dZ carry the storage
 // scales of Storage<f16> (dZ = (p - onehot) kDz for valid tokens; g is applied later).
 template <typename T>
-__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t KP, const float* __restrict__ pmax,
-                                                      int64_t ldp, const float* __restrict__ lse,
-                                                      const int64_t* __restrict__ y, int64_t ignore_index,
-                                                      const int* __restrict__ n_valid, int mean, int rows,
-                                                      int V) {
+__device__ __forceinline__ void dlogits_block(T* __restrict__ ez, int64_t KP, int64_t bx, int jb,
+                                              const float* __restrict__ pmax, int64_t ldp,
+                                              const float* __restrict__ lse, const int64_t* __restrict__ y,
+                                              int64_t ignore_index, const int* __restrict__ n_valid, int mean,
+                                              int rows, int V) {
   constexpr int kVec = 16 / sizeof(T);          // ids per piece
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int jb = blockIdx.y;
-  const int64_t q0 = 16 * (int64_t)blockIdx.x + 4 * w;
+  const int64_t q0 = 16 * bx + 4 * w;
   char* piece = (char*)ez + ((size_t)jb * KP + q0) * 1024 + l * 16;
   // All four pieces are read before any is written: HBM needs the loads in flight together. Tokens
   // at or beyond `rows` read stale data that the select below discards.
@@ -149,6 +197,21 @@ __global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_
     }
     *(uint4*)(piece + k * 1024) = *(const uint4*)outv;
   }
+}
+
+// The grid walks the (b, jb) pairs b fastest (a grid as large as their count takes one each);
+// run_if: do nothing unless *run_if != 0 (nullptr: always run).
+template <typename T>
+__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t KP, int64_t NB,
+                                                      const float* __restrict__ pmax,
+                                                      int64_t ldp, const float* __restrict__ lse,
+                                                      const int64_t* __restrict__ y, int64_t ignore_index,
+                                                      const int* __restrict__ n_valid, int mean, int rows,
+                                                      int V, const int* __restrict__ run_if) {
+  if (run_if != nullptr && *run_if == 0) return;
+  const int64_t nbx = KP / 16;
+  for (int64_t idx = blockIdx.x; idx < nbx * NB; idx += gridDim.x)
+    dlogits_block<T>(ez, KP, idx % nbx, (int)(idx / nbx), pmax, ldp, lse, y, ignore_index, n_valid, mean, rows, V);
 }
 
 // out[i][h] = sum_s part[s][i][h] (fixed order), times the dz storage scale's inverse of the

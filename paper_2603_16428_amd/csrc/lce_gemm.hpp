@@ -89,6 +89,13 @@ struct GemmArgs {
   int mode;           // DW: DwMode; STORE: 1 = fp32 split-K partials at out + split * M * ldo
   const int* n_valid; // STORE (mode 0) / DW of 16-bit types whose dz is stored unscaled: the
   int mean;           // valid-token count and reduction that give g (see Storage)
+  // LSE_BWD, target-referenced (ref != nullptr; chunk-offset, like the columns): ref[col] is the
+  // token's target logit if it has a valid label, else NaN. A token with a finite ref has its e
+  // stored relative to it instead of the slice maximum, and its partials use the same reference;
+  // every other token (ignored, label outside [0, M), padding) has its e stored as 0.
+  const float* ref;
+  const float* col_scale;  // STORE: per-column factor on the accumulators (nullptr = none)
+  const int* run_if;       // nullptr, or: the launch does nothing unless *run_if != 0
 };
 
 // K-contig tiles: logical 16-byte chunk c (0..7) of LDS row r sits in slot c ^ swz_k(r).
@@ -561,7 +568,7 @@ __device__ __forceinline__ float dw_prev_scale(const GemmArgs& g) {
 // PRELOADED (DW): the accumulators started from the tile's current dW values.
 template <typename T, int EPI, bool PRELOADED>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4][4], int mw, int nw, int split,
-                                              bool accumulate) {
+                                              bool accumulate, int n0, const char* refs_lds) {
   constexpr int kEsz = (int)sizeof(T);
   const int lane = lane_id();
   const int sub4 = 4 * (lane >> 5);
@@ -569,32 +576,58 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
   if constexpr (EPI == EPI_LSE_FWD || EPI == EPI_LSE_BWD) {
     if (mw >= g.M) return;
     const int slice = mw / kLseSlice;
+    const bool tref = EPI == EPI_LSE_BWD && g.ref != nullptr;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int col = nw + 32 * j + l32;
-      float mx = -INFINITY;
+      const bool in = col < g.N;
+      float m_ref, s = 0.f;
+      if (tref) {
+        // Target-referenced: the token's reference (the tile's references were copied to LDS while
+        // the pipeline filled). A token without one (ignored, invalid label, padding) takes +inf,
+        // so its e is exactly 0 and its partial sum 0: a backward call reports no lse, and such a
+        // token's loss does not depend on it.
+        const float ref = *(const float*)(refs_lds + 4 * (col - n0));
+        const bool keep = in && __builtin_isfinite(ref);
+        m_ref = keep ? ref : 0.f;
+        const float ml = keep ? ref * kLog2e : INFINITY;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-          if (row < g.M) mx = fmaxf(mx, acc[i][j][r]);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float ml = mx * kLog2e;
-      float s = 0.f;
+          for (int r = 0; r < 16; ++r) {
+            const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
+            const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
+            s += e;
+            acc[i][j][r] = e;
+          }
+      } else {
+        // The slice maximum as the reference.
+        float mx = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-          const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
-          s += e;
-          acc[i][j][r] = e * Storage<T>::kE;
-        }
+          for (int r = 0; r < 16; ++r) {
+            const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
+            if (row < g.M) mx = fmaxf(mx, acc[i][j][r]);
+          }
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        m_ref = mx;
+        const float ml = mx * kLog2e;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
+            const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
+            s += e;
+            acc[i][j][r] = e * Storage<T>::kE;
+          }
+      }
       s += __shfl_xor(s, 32);
-      if (col < g.N) {
-        if constexpr (EPI == EPI_LSE_BWD) {
+      if constexpr (EPI == EPI_LSE_BWD) {
+        // Every token block that holds a token of the chunk is written whole: target-referenced,
+        // the lanes of tokens at or beyond N store zeros (the dW GEMM sums over the last block).
+        if (nw + 32 * j < g.N) {
           // e blocked: the token is column l%32 of token block col/32, so this lane's piece of every
           // fragment of that block is at lane * 16; 32 ids fill the lane's pieces of two fragments.
           char* e_blk = (char*)g.out + (size_t)((nw + 32 * j) >> 5) * g.ldo * 1024 + lane * 16;
@@ -615,10 +648,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
               }
           }
         }
-        if (lane < 32) {
-          g.pmax[(size_t)slice * g.ldp + col] = mx;
-          g.psum[(size_t)slice * g.ldp + col] = s;
-        }
+      }
+      if (in && lane < 32) {
+        g.pmax[(size_t)slice * g.ldp + col] = m_ref;
+        g.psum[(size_t)slice * g.ldp + col] = s;
       }
     }
   } else if constexpr (EPI == EPI_STORE) {
@@ -631,6 +664,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     for (int j = 0; j < 4; ++j) {
       const int col = nw + 32 * j + l32;
       if (col >= g.N) continue;
+      if (g.col_scale) {
+        const float cs = g.col_scale[col];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i][j] *= cs;
+      }
       if (g.mode == 1) {
         float* o = (float*)g.out + ((size_t)split * g.N + col) * g.ldo;
 #pragma unroll
@@ -719,7 +757,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
 // same K bytes: K-pair p of K-tile t, lane half h, bytes [32 p + 16 h, +16) of the K-tile.)
 constexpr int kXbASlots = 4;
 constexpr int kXbAhead = kXbASlots - 1;
-constexpr int kXbSmem = kXbASlots * kOperandBytes;  // 128 KB
+// The A ring, then 1 KB for the tile's 256 per-token references (target-referenced LSE_BWD).
+constexpr int kXbRefs = kXbASlots * kOperandBytes;
+constexpr int kXbSmem = kXbRefs + 1024;  // 129 KB
 
 // Blocked copy of a K-contiguous source (element (n, k) at src[n * ld + k]; K a multiple of 16
 // bytes' worth): one thread per 16-byte piece. Grid: NB * KP * 64 threads.
@@ -741,9 +781,10 @@ __global__ __launch_bounds__(256) void block_k_kernel(const T* __restrict__ src,
 // Blocked copy of an MN-contiguous source (element (n, k) at src[k * ld + n]; N a multiple of 16
 // bytes' worth): block (jb, g) stages the 128 bytes' worth of K rows of K-pairs 4g .. 4g + 3 by 32
 // columns in LDS, then each thread gathers one 16-byte piece down a column. Grid: (NB, ceil(KP / 4)).
+// row_scale (nullptr = none): K row k is multiplied by row_scale[k] on the way (rounded once to T).
 template <typename T>
 __global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src, int64_t ld, int N, int K, int KP,
-                                                       T* __restrict__ dst) {
+                                                       T* __restrict__ dst, const float* __restrict__ row_scale) {
   constexpr int kEsz = (int)sizeof(T);
   constexpr int kVec = 16 / kEsz;            // elements per piece
   constexpr int kRows = 128 / kEsz;          // K rows of four K-pairs
@@ -757,7 +798,16 @@ __global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src
     const int r = t / kPieces, pc = t % kPieces;
     const int k = grp * kRows + r, n = 32 * jb + pc * kVec;
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (k < K && n < N) v = *(const u32x4*)(src + (size_t)k * ld + n);
+    if (k < K && n < N) {
+      v = *(const u32x4*)(src + (size_t)k * ld + n);
+      if (row_scale != nullptr) {
+        const float c = row_scale[k];
+        vec_t x = __builtin_bit_cast(vec_t, v);
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) x[e] = (T)((float)x[e] * c);
+        v = __builtin_bit_cast(u32x4, x);
+      }
+    }
     *(u32x4*)&tile[r][pc * kVec] = v;
   }
   __syncthreads();
@@ -775,8 +825,7 @@ __global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src
 // A checks every chunk against the K range (see Operand::offset). Splits must start at whole
 // K-tiles (k_per_split).
 template <typename T, int EPI, int AL, bool KCHECK>
-__global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs g) {
-  extern __shared__ __attribute__((aligned(1024))) char smem[];
+__device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* smem) {
   constexpr int kEsz = (int)sizeof(T);
   constexpr int kBK = kTileBytes / kEsz;
   constexpr bool kSwap = EPI == EPI_DW;
@@ -788,7 +837,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
 
   const int total = g.tiles_m * g.tiles_n * g.splits;
   int tm, rest;
-  tile_coords(blockIdx.x, total, g.tiles_m, g.group_m, tm, rest);
+  tile_coords(bid, total, g.tiles_m, g.group_m, tm, rest);
   tm = __builtin_amdgcn_readfirstlane(tm);
   rest = __builtin_amdgcn_readfirstlane(rest);
   const int tn = rest % g.tiles_n;
@@ -932,6 +981,15 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
   }
   // An odd count runs one more K-tile of zeros (past the end every load reads zeros).
   const int nk = (ke - kb + kBK - 1) / kBK;
+  // Target-referenced LSE_BWD: the tile's 256 references into LDS, one LDS-DMA load issued before
+  // the prologue's (so that none of its hand-counted waits counts it); past N it reads zeros. The
+  // first barrier of the main loop comes after this wave's wait for it.
+  const bool tref = EPI == EPI_LSE_BWD && g.ref != nullptr;
+  if (tref && w == 0) {
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc((const void*)uniform64((uint64_t)(g.ref + n0)),
+                                                __builtin_amdgcn_readfirstlane((uint32_t)max(0, g.N - n0) * 4u));
+    dma16(rr, smem + kXbRefs, (uint32_t)lane * 16u);
+  }
   if (nk > 0) {
     // Prologue: A(0 .. ahead-1), then B(0 .. 6). A(0) has landed for every wave (issued after it:
     // the other A K-tiles and 28 B loads) before its first fragments are read; the first waits at
@@ -971,7 +1029,16 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
 
-  gemm_epilogue<T, EPI, kPreload>(g, acc, mw, nw, split, accumulate);
+  gemm_epilogue<T, EPI, kPreload>(g, acc, mw, nw, split, accumulate, n0, smem + kXbRefs);
+}
+
+// One 256 x 256 tile per workgroup. With g.run_if set, the whole grid does nothing unless
+// *g.run_if is nonzero: work that a flag set on the device may or may not ask for.
+template <typename T, int EPI, int AL, bool KCHECK>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_xb_kernel(const GemmArgs g) {
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  if (g.run_if != nullptr && __builtin_amdgcn_readfirstlane(*g.run_if) == 0) return;
+  gemm_xb_tile<T, EPI, AL, KCHECK>(g, blockIdx.x, smem);
 }
 
 }  // namespace lce

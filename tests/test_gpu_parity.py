@@ -101,6 +101,61 @@ def test_ragged_shapes(lce, N, H, V, dtype, chunk):
     _check_full(lce, d, chunk_tokens=chunk)
 
 
+def _with_extreme_tokens(d, tokens):
+    """Sets, for each (token, alpha), a label and that label's weight row so that the token's
+    target logit is alpha (x . w_y = alpha, up to rounding): a large negative alpha gives the token
+    a loss far above the others, a large positive one a target far above every other logit."""
+    X = d["hidden"].double()
+    W = d["weight"].double().clone()
+    y = d["labels"].clone()
+    for k, (i, alpha) in enumerate(tokens):
+        lab = (17 * k + 5) % d["V"]
+        y[i] = lab
+        W[lab] = alpha * X[i] / float(X[i] @ X[i])
+    d = dict(d)
+    d["weight"], d["labels"] = W.to(d["weight"].dtype), y
+    return d
+
+
+# Losses of 75 (exp(z - z_target) up to e^75: finite, but above the 60 that the target-referenced
+# path accepts) and 120 (exp overflows fp32): the chunk is redone with slice-maximum references.
+# A target logit of +100 leaves every other exp(z - z_target) below fp32's range (zero or
+# subnormal), where p is that small too. Several chunks, only some of them falling back.
+@pytest.mark.parametrize("dtype", ["bf16", "fp32", "fp16"])
+@pytest.mark.parametrize("tokens,chunk", [
+    ([(5, -75.0)], 0),
+    ([(5, -120.0)], 0),
+    ([(3, 100.0), (40, 90.0)], 0),
+    ([(200, -80.0), (3, 100.0)], 64),
+])
+def test_extreme_target_logits(lce, dtype, tokens, chunk):
+    d = workloads.random_case(300, 64, 300, dtype=dtype, seed=11, w_std=0.3)
+    _check_full(lce, _with_extreme_tokens(d, tokens), chunk_tokens=chunk)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32", "fp16"])
+def test_label_outside_vocabulary(lce, dtype):
+    # Reading A4: a non-ignored label outside [0, V) cannot be reported by the call; that token's
+    # loss is NaN (so is the reduced loss) and the gradients stay finite. bf16 and fp32 drop the
+    # token from the gradients entirely: with the sum, they equal the oracle's with it ignored.
+    d = workloads.random_case(150, 64, 700, dtype=dtype, seed=21, w_std=0.3)
+    y = d["labels"].clone()
+    y[7], y[100] = d["V"] + 3, -5
+    X, W = d["hidden"].cuda(), d["weight"].cuda()
+    loss, dH, dW = lce.forward_backward(X, W, y.cuda(), d["ignore_index"], "sum", chunk_tokens=64)
+    torch.cuda.synchronize()
+    assert torch.isnan(loss).item()
+    assert torch.isfinite(dH.float()).all() and torch.isfinite(dW.float()).all()
+    if dtype != "fp16":
+        y_ref = y.clone()
+        y_ref[7] = y_ref[100] = d["ignore_index"]
+        ref = oracle.forward_backward(d["hidden"], d["weight"], y_ref, d["ignore_index"], "sum")
+        tol = TOL[dtype][1]
+        assert _rel_max_err(dH.float().cpu().numpy(), ref["dH"]) <= tol
+        assert _rel_max_err(dW.float().cpu().numpy(), ref["dW"]) <= tol
+        assert torch.all(dH[7] == 0) and torch.all(dH[100] == 0)
+
+
 @pytest.mark.parametrize("reduction", ["mean", "sum"])
 def test_reductions(lce, reduction):
     d = workloads.random_case(200, 96, 3001, seed=3, w_std=0.3)
