@@ -35,9 +35,14 @@
  *     throughout (FP32). loss and lse are fp32; grad_hidden and grad_weight have the input dtype.
  *     With FP16 the library keeps its intermediate per-logit values in fp16 under fixed power-of-two
  *     scales, so that the 1/n_valid-sized gradient entries do not underflow fp16's exponent range;
- *     the results carry the precision of fp16 outputs.
+ *     the results carry the precision of fp16 outputs. With BF16 and FP32 the backward keeps each
+ *     token's exp(z - z_target) in the input dtype (the softmax gradient then factors into a
+ *     per-token scale); a chunk holding a token whose loss exceeds 60 is redone with per-slice
+ *     maxima instead, so no intermediate value overflows.
  *   - A non-ignored label outside [0, V) is not an error the call can report (labels live on the
- *     device); its token's loss becomes NaN and it contributes no one-hot term to the gradients.
+ *     device); its token's loss becomes NaN (and so does a MEAN or SUM loss). With BF16 and FP32
+ *     the token contributes nothing to the gradients; with FP16 it contributes its softmax without
+ *     a one-hot term. The gradients stay finite either way.
  *   - MEAN with no valid token gives loss 0 and zero gradients.
  *   - Supported shapes: N, H, V >= 1 and below 2^30; H a multiple of 8 (BF16, FP16) or 4 (FP32);
  *     256 x max(H, V rounded up to 256) elements below 2^31 bytes; a chunk's blocked copies of X
