@@ -267,10 +267,8 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
 
   {
     KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(1024), 0, s, y, N, ignore_index, nvalid, flags,
-                       (int64_t)(flags ? p.chunks : 0));
-    hipLaunchKernelGGL((target_logit_kernel<T>), dim3((unsigned)cdiv(N, 4)), dim3(256), 0, s, X, W, y, N, H, V,
-                       ignore_index, tgt, tref);
+    hipLaunchKernelGGL((prepare_kernel<T>), dim3((unsigned)(cdiv(N, 4) + 1)), dim3(256), 0, s, X, W, y, N, H, V,
+                       ignore_index, tgt, tref, nvalid, flags, (int64_t)(flags ? p.chunks : 0));
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return LCE_ERR_HIP;
 

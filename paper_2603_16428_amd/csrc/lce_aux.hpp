@@ -15,34 +15,33 @@ template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf
 template <> __device__ __forceinline__ f16 from_f32<f16>(float v) { return (f16)v; }
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
-// n_valid = number of labels different from ignore_index, over all N tokens (the mean's divisor
-// is global, never per chunk). One block of 1024 threads; fixed-order tree, so deterministic. Also
-// clears the chunks' fallback flags (see combine_kernel).
-__global__ __launch_bounds__(1024) void count_valid_kernel(const int64_t* __restrict__ y, int64_t N,
-                                                           int64_t ignore_index, int* __restrict__ n_valid,
-                                                           int* __restrict__ flags, int64_t nflags) {
-  __shared__ int part[1024];
-  for (int64_t k = threadIdx.x; k < nflags; k += 1024) flags[k] = 0;
-  int c = 0;
-  for (int64_t i = threadIdx.x; i < N; i += 1024) c += (y[i] != ignore_index);
-  part[threadIdx.x] = c;
-  __syncthreads();
-  for (int s = 512; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) *n_valid = part[0];
-}
-
-// Target logit z_{i, y_i} = x_i . w_{y_i} in fp32, one wave per token. Ignored tokens get 0;
-// a label outside [0, V) gets NaN (so that the token's loss is NaN) and reads nothing. ref
-// (optional): the reference of the target-referenced logits epilogue, z_{i, y_i} for a valid label
-// and NaN otherwise.
+// The call's first kernel. Blocks 0 .. ceil(N/4) - 1: the target logit z_{i, y_i} = x_i . w_{y_i}
+// in fp32, one wave per token; ignored tokens get 0, a label outside [0, V) gets NaN (so that the
+// token's loss is NaN) and reads nothing; ref (optional) receives the reference of the
+// target-referenced logits epilogue, z_{i, y_i} for a valid label and NaN otherwise. The last
+// block: n_valid = the number of labels different from ignore_index over all N tokens (the mean's
+// divisor is global, never per chunk; fixed-order tree), and clears the chunks' fallback flags
+// (see combine_kernel). Grid: ceil(N/4) + 1 blocks of 256 threads.
 template <typename T>
-__global__ __launch_bounds__(256) void target_logit_kernel(const T* __restrict__ X, const T* __restrict__ W,
-                                                           const int64_t* __restrict__ y, int64_t N, int64_t H,
-                                                           int64_t V, int64_t ignore_index, float* __restrict__ tgt,
-                                                           float* __restrict__ ref) {
+__global__ __launch_bounds__(256) void prepare_kernel(const T* __restrict__ X, const T* __restrict__ W,
+                                                      const int64_t* __restrict__ y, int64_t N, int64_t H,
+                                                      int64_t V, int64_t ignore_index, float* __restrict__ tgt,
+                                                      float* __restrict__ ref, int* __restrict__ n_valid,
+                                                      int* __restrict__ flags, int64_t nflags) {
+  if (blockIdx.x == gridDim.x - 1) {
+    __shared__ int part[256];
+    for (int64_t k = threadIdx.x; k < nflags; k += 256) flags[k] = 0;
+    int c = 0;
+    for (int64_t i = threadIdx.x; i < N; i += 256) c += (y[i] != ignore_index);
+    part[threadIdx.x] = c;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+      if ((int)threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) *n_valid = part[0];
+    return;
+  }
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (i >= N) return;
@@ -105,11 +104,23 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const int i = blockIdx.x * kCombineTokens + t;
   float m = -INFINITY, s = 0.f;
   if (i < rows) {
-    for (int k = grp; k < slices; k += 16) {
-      const float mk = pmax[(size_t)k * ldp + i], sk = psum[(size_t)k * ldp + i];
-      const float mn = fmaxf(m, mk);
-      s = s * __expf(m - mn) + sk * __expf(mk - mn);
-      m = mn;
+    // Eight slices' partials are requested before any is merged (the merge order is unchanged).
+    constexpr int kAhead = 8;
+    for (int k0 = grp; k0 < slices; k0 += 16 * kAhead) {
+      float mk[kAhead], sk[kAhead];
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) {
+        const int k = min(k0 + 16 * u, slices - 1);
+        mk[u] = pmax[(size_t)k * ldp + i];
+        sk[u] = psum[(size_t)k * ldp + i];
+      }
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) {
+        if (k0 + 16 * u >= slices) break;
+        const float mn = fmaxf(m, mk[u]);
+        s = s * __expf(m - mn) + sk[u] * __expf(mk[u] - mn);
+        m = mn;
+      }
     }
   }
   sm[grp][t] = m;
