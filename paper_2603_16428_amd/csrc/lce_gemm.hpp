@@ -448,6 +448,46 @@ struct Operand {
     }
   }
 
+  // 16-bit MN-contig and blocked A: the fragment reads address LDS through per-lane registers that
+  // hold the whole address in the current pair of ring slots (slots 0-1 or 2-3), so that the slot
+  // within the pair, the K-pair and the block enter as the read's immediate offset and no address
+  // arithmetic sits between the MFMAs. MN: xa[i] for block i (frag[0] ^ (i << 6)); blocked: xa[0]
+  // and xa[1] for the two reads of a fragment (frag[0], frag[0] ^ 64). All plus the ring's base.
+  static constexpr int kXa = (kEsz == 2 && MN) ? (BLK ? 2 : 4) : 0;
+  uint32_t xa[kXa > 0 ? kXa : 1];
+  __device__ __forceinline__ void init_xa(uint32_t ring_base) {
+    if constexpr (kXa > 0) {
+#pragma unroll
+      for (int k = 0; k < kXa; ++k)
+        xa[k] = ring_base + (uint32_t)(frag[0] ^ (k << 6));
+    }
+  }
+  // Moves the addresses to the other pair of slots (delta = +-2 slots).
+  __device__ __forceinline__ void shift_xa(int delta) {
+    if constexpr (kXa > 0) {
+#pragma unroll
+      for (int k = 0; k < kXa; ++k) xa[k] += (uint32_t)delta;
+    }
+  }
+  // Fragment of K-pair KPR of block i in slot SIP (0, 1) of the pair that the addresses `a` point at.
+  template <int SIP, int KPR>
+  static __device__ __forceinline__ f32x4 fragment_x(const uint32_t (&a)[kXa > 0 ? kXa : 1], int i) {
+    i16x4 lo, hi;
+    if constexpr (BLK) {
+      // Block i adds 2048 i; K-pair p adds 16384 (p/2) + 256 (p%2); the second read is at frag ^ 64.
+      asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%4\n\tds_read_b64_tr_b16 %1, %3 offset:%4"
+                   : "=v"(lo), "=v"(hi)
+                   : "v"(a[0]), "v"(a[1]), "i"(SIP * kOperandBytes + 16384 * (KPR >> 1) + 256 * (KPR & 1) + 2048 * i));
+    } else {
+      asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%3\n\tds_read_b64_tr_b16 %1, %2 offset:%4"
+                   : "=v"(lo), "=v"(hi)
+                   : "v"(a[i]), "i"(SIP * kOperandBytes + (16 * KPR) * kMnRowBytes),
+                     "i"(SIP * kOperandBytes + (16 * KPR + 4) * kMnRowBytes));
+    }
+    const i16x4 v[2] = {lo, hi};
+    return __builtin_bit_cast(f32x4, v);
+  }
+
   // Fragment of K-pair p of block i from the LDS tile at `st`.
   __device__ __forceinline__ f32x4 fragment(const char* st, int p, int i, int khalf, int sw) const {
     if constexpr (!MN) {
@@ -904,6 +944,24 @@ __device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* s
 #pragma unroll
     for (int i = 0; i < 4; ++i) fa[buf][i] = opa.fragment(sa, p, i, khalf, swi[i]);
   };
+  // 16-bit MN-contig / blocked A: reads through the address registers. NEXT: the pair of slots after
+  // the current one (the addresses moved by pair_delta for these reads only).
+  constexpr bool kXread = Operand<T, AL>::kXa > 0;
+  int pair_delta = 2 * kOperandBytes;  // current pair 0-1: the next is 2 slots up, then down
+  if constexpr (kXread) opa.init_xa((uint32_t)(uintptr_t)(lds_void*)smem);
+  auto read_frags_x = [&](auto sip, auto kpr, auto next, int buf) {
+    constexpr int SIP = decltype(sip)::value, KPR = decltype(kpr)::value;
+    if constexpr (decltype(next)::value) {
+      uint32_t a[Operand<T, AL>::kXa > 0 ? Operand<T, AL>::kXa : 1];
+#pragma unroll
+      for (int k = 0; k < Operand<T, AL>::kXa; ++k) a[k] = opa.xa[k] + (uint32_t)pair_delta;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[buf][i] = Operand<T, AL>::template fragment_x<SIP, KPR>(a, i);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[buf][i] = Operand<T, AL>::template fragment_x<SIP, KPR>(opa.xa, i);
+    }
+  };
   // Fragment reads issued as inline assembly are invisible to the compiler's wait insertion: at
   // the start of each section wait for all earlier LDS traffic (the previous section's reads, long
   // since done), with the fragment registers as operands so that no MFMA moves above the wait.
@@ -951,8 +1009,19 @@ __device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* s
     const int ktp = kt + (s >> 2);
     if constexpr (p == 3) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAWait) : "memory");
     sync_frags();
-    if constexpr (p == 3) read_frags(ktp + 1, 0, (s + 1) & 1);
-    else read_frags(ktp, p + 1, (s + 1) & 1);
+    if constexpr (kXread) {
+      // Section s reads K-tile kt + s/4 (slot s/4 of the current pair), or at p == 3 the next
+      // K-tile: kt + 1 (slot 1) from section 3, kt + 2 (slot 0 of the next pair) from section 7.
+      using I = std::integral_constant<int, 0>;
+      using One = std::integral_constant<int, 1>;
+      if constexpr (s == 3) read_frags_x(One{}, I{}, std::false_type{}, (s + 1) & 1);
+      else if constexpr (s == 7) read_frags_x(I{}, I{}, std::true_type{}, (s + 1) & 1);
+      else read_frags_x(std::integral_constant<int, (s >> 2)>{}, std::integral_constant<int, p + 1>{},
+                        std::false_type{}, (s + 1) & 1);
+    } else {
+      if constexpr (p == 3) read_frags(ktp + 1, 0, (s + 1) & 1);
+      else read_frags(ktp, p + 1, (s + 1) & 1);
+    }
     // Loads retire in issue order, so a B load waits for every A load issued before it. With A
     // K-contiguous (W, streamed from HBM) the section issues its B fragments first (measured 4%
     // faster on the logits GEMM); with A MN-contiguous (dZ^T) the order made no difference.
@@ -1013,7 +1082,11 @@ __device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* s
     load_b(5, std::integral_constant<int, 5>{});
     load_b(6, std::integral_constant<int, 6>{});
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(8 * (kXbAhead - 1) + 28) : "memory");
-    read_frags(0, 0, 0);
+    if constexpr (kXread) {
+      read_frags_x(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, std::false_type{}, 0);
+    } else {
+      read_frags(0, 0, 0);
+    }
     for (int kt = 0; kt < nk; kt += 2) {
       section(kt, std::integral_constant<int, 0>{});
       section(kt, std::integral_constant<int, 1>{});
@@ -1023,6 +1096,10 @@ __device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* s
       section(kt, std::integral_constant<int, 5>{});
       section(kt, std::integral_constant<int, 6>{});
       section(kt, std::integral_constant<int, 7>{});
+      if constexpr (kXread) {
+        opa.shift_xa(pair_delta);
+        pair_delta = -pair_delta;
+      }
     }
     // Loads past the end may still be in flight (they target no memory); their LDS and registers
     // must not be reused before they retire.
