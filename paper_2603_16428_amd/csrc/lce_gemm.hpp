@@ -300,7 +300,7 @@ struct Operand {
   int64_t ld;
   int kb, ke;         // K range of this split
   // Byte offset of load j within a K-tile = row_off + j * row_step + (slot_x ^ xor_j(j)): a lane
-  // term, a uniform term and a compile-time XOR. Two registers per lane instead of eight offsets.
+  // term, a uniform term and a compile-time XOR (the kernel forms the eight per-lane terms once).
   uint32_t row_off, slot_x, row_step;
   int frag[4];        // per 32-row block: this lane's LDS byte offset at K-pair 0
   __amdgpu_buffer_rsrc_t rsrc_k;  // K-contig: one descriptor for the whole run
@@ -410,19 +410,15 @@ struct Operand {
     }
   }
 
-  // Byte offset of load j of K-tile t, in two parts: a per-lane part, formed by one v_xad_u32 where
-  // it is used (hoisted out of the main loop, the sixteen offsets of two operands would outgrow the
-  // registers and be spilled, and spill traffic would upset the vmcnt waits), and a uniform part in
-  // soffset: j row_step plus, K-contig, the K-tile's start (kOOB for a K-tile at or past ke). A
-  // chain of dependent address instructions in front of each load stalls the in-order issue, and
-  // the MFMAs queued behind it, for tens of cycles per load. K-contig, this reads whole K-tiles:
-  // only for K ranges made of whole K-tiles, or rows whose padding up to the next K-tile is zeros
-  // (or meets zeros in the other operand); otherwise offset() below checks every chunk.
-  __device__ __forceinline__ uint32_t lane_offset(int j) const {
-    uint32_t o;
-    asm volatile("v_xad_u32 %0, %1, %2, %3" : "=v"(o) : "v"(slot_x), "s"(xor_j(j)), "v"(row_off));
-    return o;
-  }
+  // Byte offset of load j of K-tile t, in two parts: a per-lane part, computed once per tile for
+  // the eight loads of a K-tile and held in registers through the main loop (lane_offset), and a
+  // uniform part in soffset: j row_step plus, K-contig, the K-tile's start (kOOB for a K-tile at or
+  // past ke). Address arithmetic in front of each load stalls the in-order issue, and the MFMAs
+  // queued behind it; with operand B straight to registers the eight lane offsets fit beside the
+  // pipeline without spills (a build test checks). K-contig, this reads whole K-tiles: only for K
+  // ranges made of whole K-tiles, or rows whose padding up to the next K-tile is zeros (or meets
+  // zeros in the other operand); otherwise offset() below checks every chunk.
+  __device__ __forceinline__ uint32_t lane_offset(int j) const { return (slot_x ^ xor_j(j)) + row_off; }
   __device__ __forceinline__ uint32_t uniform_offset(int t, int j) const {
     uint32_t o = (uint32_t)j * row_step;
     if constexpr (!MN) {
@@ -905,6 +901,9 @@ __device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* s
   const int q0 = kb * kEsz / 32;
   const int qend = ((ke - kb) * kEsz + 31) / 32;
 
+  uint32_t aoff[8];  // per-lane parts of the eight loads of an A K-tile
+#pragma unroll
+  for (int j = 0; j < 8; ++j) aoff[j] = opa.lane_offset(j);
   // Quarter pc of A K-tile t (loads 2 pc, 2 pc + 1) into ring slot t % 4.
   auto load_a_q = [&](int t, auto pc) {
     constexpr int pq = decltype(pc)::value;
@@ -913,7 +912,7 @@ __device__ __forceinline__ void gemm_xb_tile(const GemmArgs& g, int bid, char* s
 #pragma unroll
     for (int j = 2 * pq; j < 2 * pq + 2; ++j) {
       if constexpr (KCHECK && AL == A_K) dma16(r, st + j * 1024, opa.offset(t, j));
-      else dma16(r, st + j * 1024, opa.lane_offset(j), opa.uniform_offset(t, j));
+      else dma16(r, st + j * 1024, aoff[j], opa.uniform_offset(t, j));
     }
   };
   auto load_a = [&](int t) {
