@@ -9,8 +9,11 @@ library on its launch stream), the forward-only rate (loss without gradients, 2*
 with the final RMSNorm fused in front (lce_rmsnorm_forward_backward), a training step of the output
 layer with host-resident weights and its hiding factor (lce_head_train_step), peak
 device memory against a materialised-logits PyTorch baseline, the median and fastest single step,
-the three contraction shapes of one chunk as plain hipBLASLt GEMMs (context), and the float64 CPU
-oracle timed on a bounded sample of the same workload.
+the rate of the W streams (W's bytes per logits / dH launch over its duration), the three
+contraction shapes of one chunk as plain hipBLASLt GEMMs (context), the steps of the other
+workloads (Qwen2.5-7B, Mistral-Large, the small one; extra keys, not the headline), and the float64
+CPU oracle timed on one whole forward + backward of the same workload, with the host's CPU model,
+sockets, cores and BLAS library.
 """
 from __future__ import annotations
 
@@ -85,22 +88,50 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(d, tokens: int):
-    """The float64 oracle, as it stands, on the first `tokens` tokens (all of V and H)."""
-    import oracle
+def host_info():
+    """The host the CPU baseline runs on: CPU model, sockets, usable cores, BLAS library and threads."""
+    model, sockets = None, set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                k, _, v = line.partition(":")
+                k, v = k.strip(), v.strip()
+                if k == "model name" and model is None:
+                    model = v
+                elif k == "physical id":
+                    sockets.add(v)
+    except OSError:
+        pass
+    blas = {}
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # threadpoolctl missing: report the affinity mask
-        threads = len(os.sched_getaffinity(0))
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = {"library": i.get("internal_api"), "version": i.get("version"),
+                        "threads": int(i.get("num_threads", 1))}
+                break
+    except Exception:  # threadpoolctl missing
+        pass
+    return {"cpu_model": model, "sockets": len(sockets) or None, "affinity_cores": len(os.sched_getaffinity(0)),
+            "blas": blas}
+
+
+def cpu_baseline(d, tokens: int):
+    """The float64 oracle, as it stands, on the first `tokens` tokens (all of V and H): by default
+    the whole workload, one complete forward + backward."""
+    import oracle
+    info = host_info()
+    threads = info["blas"].get("threads") or info["affinity_cores"]
     n = min(tokens, d["N"])
     X, y = d["hidden"][:n], d["labels"][:n]
     t = time.perf_counter()
     oracle.forward_backward(X, d["weight"], y, d["ignore_index"], d["reduction"], rows_per_block=256)
     dt = time.perf_counter() - t
+    what = "all" if n == d["N"] else f"first {n} of"
     return {"value": n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} of {d['N']} tokens of {d['name']} (full V={d['V']}, H={d['H']}), float64 "
-                      f"forward+backward incl. upcast, {dt:.1f} s"}
+            "sample": f"{what} {d['N']} tokens of {d['name']} (V={d['V']}, H={d['H']}): one float64 "
+                      f"forward+backward (loss, dH, dW) incl. the upcast, {dt:.1f} s",
+            "seconds": round(dt, 2), "host": info}
 
 
 def materialised_baseline(X, W, y, ignore_index, reduction, reps=3):
@@ -129,6 +160,45 @@ def materialised_baseline(X, W, y, ignore_index, reduction, reps=3):
     return peak, min(times)
 
 
+def other_workload(lce, name, dtype_override, steps=10, warmup=3):
+    """One more workload's step, timed like the main one (fewer steps): ms, tokens/s, fraction of
+    the dense peak, and each contraction's share."""
+    import torch
+    import workloads
+    t0 = time.time()
+    d = workloads.make_inputs(name, seed=0, dtype=dtype_override)
+    N, H, V = d["N"], d["H"], d["V"]
+    dev = torch.device("cuda:0")
+    X, W, y = d["hidden"].to(dev), d["weight"].to(dev), d["labels"].to(dev)
+    plan = lce.plan_info(N, H, V, X.dtype, True, 0)
+    ws = torch.empty(plan["workspace_bytes"], dtype=torch.uint8, device=dev)
+    out = (torch.empty(1, dtype=torch.float32, device=dev), torch.empty_like(X), torch.empty_like(W))
+    for _ in range(warmup):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
+    torch.cuda.synchronize()
+    lce.timing_enable(True)
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
+    b.record(stream)
+    torch.cuda.synchronize()
+    kern = lce.timing_read()
+    lce.timing_enable(False)
+    ms = a.elapsed_time(b) / steps
+    peak = PEAK_FP32_TFLOPS if X.dtype == torch.float32 else PEAK_BF16_TFLOPS
+    frac = 6.0 * N * H * V / (ms * 1e-3) / 1e12 / peak
+    rec = {"N": N, "H": H, "V": V, "dtype": d["dtype"], "reduction": d["reduction"], "steps": steps,
+           "chunk_tokens": plan["chunk_tokens"], "chunks": plan["chunks"], "dh_splits": plan["dh_splits"],
+           "ms_per_step": round(ms, 4), "tokens_per_s": round(N / (ms * 1e-3), 1), "mfma_peak_frac": round(frac, 4),
+           "kernels_ms_per_step": {k: round(v[0] / steps, 4) for k, v in kern.items() if v[1]}}
+    log(f"{name}: {ms:.3f} ms/step ({100 * frac:.1f}% of peak; inputs {time.time() - t0:.0f} s)")
+    del X, W, y, ws, out
+    torch.cuda.empty_cache()
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -138,7 +208,9 @@ def main():
     ap.add_argument("--dtype", choices=["bf16", "fp16", "fp32"], default=None,
                     help="override the workload's element type (same draws, rounded to this type)")
     ap.add_argument("--chunk", type=int, default=0, help="tokens per chunk (0 = automatic)")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=3072)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=0, help="oracle tokens (0 = the whole workload)")
+    ap.add_argument("--other-workloads", default="qwen25_7b,mistral_large,small_bf16",
+                    help="comma-separated workloads whose step is also timed (extra keys); empty for none")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
     ap.add_argument("--no-rmsnorm", action="store_true", help="skip timing the variant with the final RMSNorm")
@@ -180,7 +252,10 @@ def main():
     out = (torch.empty(1, dtype=torch.float32, device=dev), torch.empty_like(X), torch.empty_like(W))
     lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
     torch.cuda.synchronize()
-    lce_peak = torch.cuda.max_memory_allocated() - base
+    # The library allocates nothing: its footprint is the workspace and outputs the caller passes.
+    # (The allocator's own figure rounds the workspace's segment up to 2 MiB.)
+    lce_alloc = torch.cuda.max_memory_allocated() - base
+    lce_peak = sum(t.numel() * t.element_size() for t in (ws,) + out)
     ws_keep = ws
 
     for _ in range(args.warmup):
@@ -222,7 +297,17 @@ def main():
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(wl_name, dom), "kernel": dom,
                 "per_launch_flops": per_launch_flops, "avg_launch_ms": dom_ms / dom_launches,
-                "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()}}
+                "all_kernels_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in kern.items()},
+                "gemm_frac": {k: round(2.0 * N * H * V * args.steps / (kern[k][0] * 1e-3) / 1e12 / peak, 4)
+                              for k in gemm_kinds}}
+    # The W streams: both the logits and the dH contraction read all of W once per launch (V x H of
+    # the dtype); their rate is W's bytes over the launch's duration.
+    w_bytes = V * H * X.element_size()
+    w_stream = {k: round(w_bytes / (kern[k][0] / kern[k][1] * 1e-3) / 1e9, 1)
+                for k in ("logits_lse_gemm", "dh_gemm")}
+    w_stream.update({"unit": "GB/s", "w_bytes_per_launch": w_bytes, "launches_per_step": chunks,
+                     "hbm_peak_gbs": PEAK_HBM_GBS})
+    log("W streams: " + ", ".join(f"{k} {v}" for k, v in w_stream.items()))
 
     # Context: the three contraction shapes of one chunk as plain hipBLASLt GEMMs (torch.mm, 2-D
     # operands; no epilogue work, no log-sum-exp, no dlogits).
@@ -319,7 +404,7 @@ def main():
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
 
-    memory = {"lce_peak_bytes": int(lce_peak)}
+    memory = {"lce_peak_bytes": int(lce_peak), "lce_allocator_peak_bytes": int(lce_alloc)}
     if not args.no_memory:
         del ws, ws_keep
         torch.cuda.empty_cache()
@@ -339,12 +424,17 @@ def main():
         "config": {"workload": wl_name,
                    "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
-        "roofline": roofline, "forward_only": forward_only, "rmsnorm_fused": rmsnorm, "head_train_step": head,
-        "memory": memory, "hipblaslt_context": blas,
+        "roofline": roofline, "w_stream": w_stream, "forward_only": forward_only, "rmsnorm_fused": rmsnorm,
+        "head_train_step": head, "memory": memory, "hipblaslt_context": blas,
     }
+    others = [w for w in args.other_workloads.split(",") if w]
+    if others:
+        del X, W, out
+        torch.cuda.empty_cache()
+        result["other_workloads"] = {w: other_workload(lce, w, args.dtype) for w in others}
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host cores ...")
-        result["cpu_baseline"] = cpu_baseline(d, args.cpu_sample_tokens)
+        result["cpu_baseline"] = cpu_baseline(d, args.cpu_sample_tokens or d["N"])
     print(json.dumps(result), flush=True)
 
 

@@ -77,21 +77,67 @@ typedef enum { LCE_REDUCTION_NONE = 0, LCE_REDUCTION_MEAN = 1, LCE_REDUCTION_SUM
  * Bytes of device workspace needed by lce_forward (with_backward = 0) or lce_forward_backward
  * (with_backward = 1) for these sizes. chunk_tokens is the number of tokens processed per chunk
  * (0 = automatic: with backward, the largest multiple of 64 not above min(H, ceil(N/2)), at least
- * 64; forward only, all N tokens up to 16384, else chunks of 16384 or the backward size if larger;
+ * 64, raised to ceil(N / limit) rounded up to 64 when that keeps the chunk count within dW's carry
+ * limit (BF16 4, FP16 9; see lce_plan_info) and is at most 2 H; forward only, all N tokens up to
+ * 16384, else chunks of 16384 or the backward size if larger;
  * a nonzero value smaller than N must be a multiple of 64). The workspace holds
  * O(chunk_tokens * (V + H) + N) elements with backward (one chunk's logits-shaped buffer, two
- * rearranged copies of the chunk's hidden rows, per-token vectors) and O(chunk_tokens * (V / 64 +
- * H) + N) forward only (per-slice partials instead); the N x V logits never exist. Returns 0 for
+ * rearranged copies of the chunk's hidden rows, per-token vectors), plus V x H fp32 when dW is
+ * carried across chunks in fp32 (see lce_plan_info), and O(chunk_tokens * (V / 64 + H) + N)
+ * forward only (per-slice partials instead); the N x V logits never exist. Returns 0 for
  * invalid arguments.
  */
 size_t lce_workspace_size(int64_t N, int64_t H, int64_t V, int dtype, int with_backward,
                           int64_t chunk_tokens);
 
+/*
+ * How a call with these arguments will run (host-side planning only: nothing is launched), for
+ * callers and tests that need to know which path the step takes.
+ *   chunk_tokens, chunks     : tokens per chunk and number of chunks.
+ *   dh_splits                : backward only: the vocabulary is split this many ways in each chunk's
+ *                              dH contraction when its tile grid would not fill the device (the splits'
+ *                              fp32 partials are then summed in a fixed order); 1 = the contraction
+ *                              stores dH directly. 0 for a forward-only plan.
+ *   target_referenced        : backward with BF16 or FP32: exp(z - z_target) is kept per logit (the
+ *                              slice-maximum path is taken only by chunks whose fallback flag is set).
+ *   dw_fp32_carry            : backward with BF16 / FP16 and more chunks than the type's carry limit
+ *                              (BF16 4, FP16 9): dW's sum over chunks is carried in an fp32 accumulator
+ *                              of V x H in the workspace instead of in dW itself. Each chunk boundary
+ *                              rounds a 16-bit running sum once (at most the unit roundoff u relative),
+ *                              so c chunks add up to (c - 1) u; the limits keep that, with the rounding
+ *                              of the stored exponentials and of the output, within 2e-2 (BF16,
+ *                              u = 2^-8) and 5e-3 (FP16, u = 2^-11) of max|dW|.
+ *   workspace_bytes          : lce_workspace_size(...) of the same arguments.
+ *   fallback_flags_offset    : backward only: byte offset in the workspace of `chunks` int32 flags.
+ *                              After a call has completed, flag c is nonzero if and only if chunk c
+ *                              was redone with slice-maximum references (some token's loss above 60,
+ *                              or inputs that are not finite); each call clears them first.
+ * Returns LCE_ERR_INVALID_ARGUMENT for a null `info` and otherwise the status lce_forward /
+ * lce_forward_backward would return for these sizes (info untouched unless LCE_OK).
+ */
+typedef struct {
+  int64_t chunk_tokens;
+  int64_t chunks;
+  int32_t dh_splits;
+  int32_t target_referenced;
+  int32_t dw_fp32_carry;
+  int32_t reserved;
+  size_t workspace_bytes;
+  size_t fallback_flags_offset;
+} lce_plan_info_t;
+lce_status_t lce_plan_info(int64_t N, int64_t H, int64_t V, int dtype, int with_backward,
+                           int64_t chunk_tokens, lce_plan_info_t* info);
+
 /* The chunk size lce_forward_backward uses for chunk_tokens = 0 (automatic), or 0 if invalid. */
 int64_t lce_auto_chunk_tokens(int64_t N, int64_t H, int64_t V, int dtype);
 
 /*
- * Forward only: the loss, and optionally each token's log-sum-exp.
+ * Forward only: the loss, and optionally each token's log-sum-exp. The projection fused with the
+ * loss without the N x V logits (Section 3.3, paragraph "Optimized Triton Kernels"); the per-token
+ * loss and lse serve evaluation, where no gradient is wanted.
+ *   dtype      : an lce_dtype_t value; reduction: an lce_reduction_t value (NONE, MEAN or SUM). Both
+ *                are passed as int throughout this header so that any value a caller passes is
+ *                well defined and an unknown one is rejected (LCE_ERR_INVALID_ARGUMENT).
  *   loss : device fp32, [1] for MEAN/SUM, [N] for NONE (per-token losses, 0 for ignored tokens).
  *   lse  : device fp32 [N], or NULL. Filled for every token, ignored ones included.
  * Performs 2*N*H*V flops of contraction.
@@ -104,7 +150,11 @@ lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* 
 
 /*
  * Forward and backward: the reduced loss and its gradients with respect to hidden and weight
- * (upstream gradient 1; scale both outputs for another upstream value).
+ * (upstream gradient 1; scale both outputs for another upstream value). This is the fused step of
+ * Section 3.3 (paragraph "Optimized Triton Kernels"): the gradients are produced token chunk by
+ * token chunk in the same call, so that only one chunk's logits-shaped buffer ever exists.
+ * chunk_tokens is the chunk size (the paper fixes none; 0 picks it automatically, see
+ * lce_workspace_size): a memory-for-time knob for the caller.
  *   reduction   : MEAN or SUM (NONE returns LCE_ERR_INVALID_ARGUMENT).
  *   loss        : device fp32 [1].
  *   grad_hidden : device [N,H] of dtype; grad_weight: device [V,H] of dtype.

@@ -74,7 +74,7 @@ int64_t cdiv(int64_t x, int64_t m) { return (x + m - 1) / m; }
 
 struct Plan {
   int64_t N = 0, H = 0, V = 0;
-  int esz = 0;
+  int esz = 0, dtype = 0;
   bool backward = false;
   // Backward with target-referenced e (bf16, fp32): the logits epilogue stores exp(z - z_target),
   // combine folds the one-hot term into e and leaves a per-token factor for the dH epilogue and
@@ -86,6 +86,9 @@ struct Plan {
   int64_t slices = 0;
   int dh_splits = 1;
   int64_t dh_kps = 0;             // K (vocabulary) per dH split, multiple of the K-tile
+  // dW's running sum over chunks in an fp32 accumulator instead of dW's own 16-bit type (more
+  // chunks than carry_chunks() allows for the type).
+  bool dw_acc32 = false;
   // Fragment-blocked copies of a chunk's X: operand B of the logits GEMM (columns = tokens,
   // K = H) and of the dW GEMM (columns = H, K = tokens): column blocks and K-pairs per block.
   int64_t xk_nb = 0, xk_kp = 0, xm_nb = 0, xm_kp = 0;
@@ -94,7 +97,7 @@ struct Plan {
   int64_t ez_nb = 0, ez_kp = 0;
   // workspace offsets (bytes)
   size_t o_nvalid = 0, o_tgt = 0, o_lse = 0, o_tl = 0, o_pmax = 0, o_psum = 0, o_e = 0, o_dhp = 0;
-  size_t o_scale = 0, o_flags = 0, o_ref = 0;
+  size_t o_scale = 0, o_flags = 0, o_ref = 0, o_acc32 = 0;
   size_t o_xk = 0, o_xm = 0;
   size_t total = 0;
 };
@@ -117,6 +120,14 @@ int num_cus() {
 
 constexpr int64_t kFwdChunk = 16384;  // automatic forward chunk (a multiple of 64)
 
+// Chunks up to which dW's running sum may be carried in dW's own 16-bit type. Each boundary
+// between chunks rounds the running sum once (relative error at most the unit roundoff u, on a
+// partial sum of about the size of the final one), so c chunks add at most (c - 1) u; with the
+// rounding of e' and of the output (2 u) the total stays within the gradient bar of the type
+// (bf16: 2e-2 = 5.1 u with u = 2^-8, so c <= 4; fp16: 5e-3 = 10.2 u with u = 2^-11, so c <= 9).
+// Beyond it the sum is carried in an fp32 accumulator of V x H in the workspace.
+int carry_chunks(int esz, int dtype) { return esz == 4 ? 0 : dtype == LCE_DTYPE_BF16 ? 4 : 9; }
+
 int64_t auto_chunk(int64_t N, int64_t H) {
   const int64_t half = cdiv(N, 2);
   int64_t nc = std::min(H, half) / 64 * 64;
@@ -134,6 +145,7 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   p.N = N; p.H = H; p.V = V;
   p.esz = dtype == LCE_DTYPE_FP32 ? 4 : 2;
   p.backward = backward;
+  p.dtype = dtype;
   p.tref = backward && dtype != LCE_DTYPE_FP16;
   if (H % (16 / p.esz) != 0) return LCE_ERR_UNSUPPORTED;
   // Automatic chunks: a training step keeps one chunk's e/dZ, so its chunks stay small; a forward
@@ -143,6 +155,16 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
                : backward      ? auto_chunk(N, H)
                : N <= kFwdChunk ? N
                                 : std::max(auto_chunk(N, H), kFwdChunk);
+  // An automatic backward chunk grows, when that keeps the chunk count within the type's carry
+  // limit, up to 2 H tokens: its e buffer then grows by less than the fp32 accumulator (V x H x 4
+  // bytes) it makes unnecessary.
+  if (chunk_tokens == 0 && backward) {
+    const int lim = carry_chunks(p.esz, dtype);
+    if (lim > 0 && cdiv(N, nc) > lim) {
+      const int64_t grown = round_up(cdiv(N, lim), 64);
+      if (grown <= 2 * H) nc = grown;
+    }
+  }
   if (nc >= N) nc = N;
   else if (nc % 64 != 0) return LCE_ERR_INVALID_ARGUMENT;
   p.nc = nc;
@@ -182,6 +204,7 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
     }
     p.dh_splits = best_s;
     p.dh_kps = cdiv(kblocks, best_s) * kbk;
+    p.dw_acc32 = p.esz == 2 && p.chunks > carry_chunks(p.esz, dtype);
   }
 
   size_t off = 0;
@@ -204,6 +227,7 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
     p.o_ref = take((size_t)N * 4);  // used by target-referenced plans (kept for all: one layout per element size)
     p.o_flags = take((size_t)p.chunks * 4);
     if (p.dh_splits > 1 || dx_f32) p.o_dhp = take((size_t)p.dh_splits * p.nc * H * 4);
+    if (p.dw_acc32) p.o_acc32 = take((size_t)V * H * 4);
   }
   p.total = off;
   return LCE_OK;
@@ -263,6 +287,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
   float* scale = p.backward ? (float*)(ws + p.o_scale) : nullptr;
   float* tref = p.tref ? (float*)(ws + p.o_ref) : nullptr;
   int* flags = p.backward ? (int*)(ws + p.o_flags) : nullptr;
+  float* acc32 = p.dw_acc32 ? (float*)(ws + p.o_acc32) : nullptr;
   const int mean = reduction == LCE_REDUCTION_MEAN;
 
   {
@@ -391,9 +416,13 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     gw.splits = 1; gw.k_per_split = (int)round_up(rows, kTileBytes / p.esz);
     gw.group_m = 4;
     gw.out = dW; gw.ldo = H;
-    gw.mode = c == 0 ? DW_STORE : DW_ACCUMULATE;
-    gw.n_valid = nvalid; gw.mean = mean;
     const bool last = c == p.chunks - 1;
+    gw.mode = c == 0 ? DW_STORE : DW_ACCUMULATE;
+    if (acc32) {
+      gw.acc32 = acc32;
+      gw.mode = c == 0 ? DW_ACC32_FIRST : last ? DW_ACC32_LAST : DW_ACC32_MID;
+    }
+    gw.n_valid = nvalid; gw.mean = mean;
     if (hook && last) {
       if (hipEventRecord(hook->dh_done, s) != hipSuccess) return LCE_ERR_HIP;
       const int64_t tiles = cdiv(V, kTile);
@@ -407,6 +436,7 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
           gb.A = ez + 32 * r0;          // blocked: vocabulary id r0 starts 32 r0 elements in
           gb.M = (int)(r1 - r0);
           gb.out = dW + r0 * H;
+          if (gb.acc32) gb.acc32 += r0 * H;
           KernelTimer t(T_DW, s);
           if (launch_gemm<T, EPI_DW, A_BLK>(gb, s) != hipSuccess) return LCE_ERR_HIP;
         }
@@ -630,6 +660,23 @@ int64_t lce_auto_chunk_tokens(int64_t N, int64_t H, int64_t V, int dtype) {
   lce::Plan p;
   if (lce::make_plan(N, H, V, dtype, true, 0, p, false) != LCE_OK) return 0;
   return p.nc;
+}
+
+lce_status_t lce_plan_info(int64_t N, int64_t H, int64_t V, int dtype, int with_backward, int64_t chunk_tokens,
+                           lce_plan_info_t* info) {
+  if (!info) return LCE_ERR_INVALID_ARGUMENT;
+  lce::Plan p;
+  const lce_status_t st = lce::make_plan(N, H, V, dtype, with_backward != 0, chunk_tokens, p, true);
+  if (st != LCE_OK) return st;
+  std::memset(info, 0, sizeof(*info));
+  info->chunk_tokens = p.nc;
+  info->chunks = p.chunks;
+  info->dh_splits = p.backward ? p.dh_splits : 0;
+  info->target_referenced = p.tref ? 1 : 0;
+  info->dw_fp32_carry = p.dw_acc32 ? 1 : 0;
+  info->workspace_bytes = p.total;
+  info->fallback_flags_offset = p.backward ? p.o_flags : 0;
+  return LCE_OK;
 }
 
 lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* labels, int64_t N, int64_t H,

@@ -79,13 +79,17 @@ __global__ __launch_bounds__(256) void prepare_kernel(const T* __restrict__ X, c
 //               partials were taken relative to z_target, so S = sum_v exp(z_v - z_target) =
 //               exp(lse - z_target) is the merged sum. dZ = g (p - onehot) = (g / S) (e - S onehot):
 //               the factor is g / S (0 for other tokens) and the label's entry of e becomes e - S.
-//               A token whose S exceeds kTrefMaxSum (loss above 60), or is not finite or below the
-//               target's own term 1 (inputs that are not finite), sets *flag: its e may have
-//               overflowed, so the chunk is redone with slice-maximum references.
+//               A token whose S exceeds kTrefMaxSum (loss above 60) or is not at least kTrefMinSum
+//               (NaN included: inputs that are not finite) sets *flag: its e may have overflowed,
+//               so the chunk is redone with slice-maximum references. The lower bound is loose on
+//               purpose: the target's own term is exp(z_y - z_target) = 1 only up to the difference
+//               between the GEMM's and the fp32 dot's rounding of z_y, so a confident token
+//               (p_y close to 1) has S slightly below 1 as often as above it.
 //   CMB_SLICE : dlogits forms dZ with g inside; the factor is 1.
 // run_if: do nothing unless *run_if != 0 (nullptr: always run).
 enum CombineMode { CMB_FORWARD = 0, CMB_TREF = 1, CMB_SLICE = 2 };
 constexpr float kTrefMaxSum = 1.1420073898e26f;  // exp(60)
+constexpr float kTrefMinSum = 0.5f;
 constexpr int kCombineTokens = 16;
 template <typename T>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ pmax, const float* __restrict__ psum,
@@ -139,7 +143,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
       float sc = 0.f;
       if (lab != ignore_index && lab >= 0 && lab < V) {
         const float sum = S * __expf(M - tgt[i]);  // every m_t is tgt[i] here, so this is S
-        if (sum >= 1.f && sum <= kTrefMaxSum) {  // (the target's own term is 1; NaN fails too)
+        if (sum >= kTrefMinSum && sum <= kTrefMaxSum) {  // (NaN fails both)
           const int nv = *n_valid;
           const float g = mean ? (nv > 0 ? 1.f / (float)nv : 0.f) : 1.f;
           sc = g / sum;

@@ -70,7 +70,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 enum Epilogue { EPI_LSE_FWD = 0, EPI_LSE_BWD = 1, EPI_STORE = 2, EPI_DW = 3 };
 // Layouts of operand A: K-contiguous, MN-contiguous, fragment-blocked (MN pieces, see Operand).
 enum ALayout { A_K = 0, A_MN = 1, A_BLK = 2 };
-enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1 };
+// DW epilogue: the first chunk writes dW, later ones add to it (the running sum carried in dW's own
+// type); or, with an fp32 cross-chunk accumulator (acc32), the first chunk writes acc32, the middle
+// ones add to it and the last one adds and writes dW.
+enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1, DW_ACC32_FIRST = 2, DW_ACC32_MID = 3, DW_ACC32_LAST = 4 };
 
 struct GemmArgs {
   const void* A;
@@ -96,6 +99,7 @@ struct GemmArgs {
   const float* ref;
   const float* col_scale;  // STORE: per-column factor on the accumulators (nullptr = none)
   const int* run_if;       // nullptr, or: the launch does nothing unless *run_if != 0
+  float* acc32;            // DW with mode DW_ACC32_*: fp32 accumulator [M, ldo]
 };
 
 // K-contig tiles: logical 16-byte chunk c (0..7) of LDS row r sits in slot c ^ swz_k(r).
@@ -673,13 +677,16 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
 #pragma unroll
             for (int i = 0; i < 4; ++i) store_frag32<T>(e_blk + (size_t)((mw + 32 * i) >> 4) * 1024, acc[i][j]);
           } else {
+            // fp32: a K-pair is 8 ids, half of it per lane half. The dH GEMM reads every K-pair that
+            // holds an id below M whole, so such a K-pair is stored whole: its ids at or beyond M
+            // hold exp = 0 here, and nothing stale from the workspace reaches the contraction.
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                const int row = mw + 32 * i + 8 * q + sub4;
-                if (row < g.M)
-                  store4((T*)(e_blk + (size_t)((mw + 32 * i + 8 * q) >> 3) * 1024), acc[i][j][4 * q],
+                const int kp_row = mw + 32 * i + 8 * q;
+                if (kp_row < g.M)
+                  store4((T*)(e_blk + (size_t)(kp_row >> 3) * 1024), acc[i][j][4 * q],
                          acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
               }
           }
@@ -740,6 +747,38 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     // DW, swapped layout: lane owns rows mw + 32i + l%32 and 4 consecutive columns per (j, q).
     // N (the output pitch) is a multiple of 4 here, so a 4-column group is all in or all out.
     const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
+    if (g.mode >= DW_ACC32_FIRST) {
+      // fp32 cross-chunk accumulator: acc32 (+)= sc * C, or at the last chunk dW = acc32 + sc * C
+      // rounded once. A row's sixteen 16-byte pieces are requested together before any is used.
+      const bool read = g.mode != DW_ACC32_FIRST, last = g.mode == DW_ACC32_LAST;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = mw + 32 * i + l32;
+        if (row >= g.M) continue;
+        float* a = g.acc32 + (size_t)row * g.ldo;
+        T* o = (T*)g.out + (size_t)row * g.ldo;
+        f32x4 base[4][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            base[j][q] = (read && col < g.N) ? *(const f32x4*)(a + col) : (f32x4){};
+          }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = nw + 32 * j + 8 * q + sub4;
+            if (col >= g.N) continue;
+            const f32x4 v = base[j][q] + sc * (f32x4){acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                                      acc[i][j][4 * q + 3]};
+            if (last) store4(o + col, v[0], v[1], v[2], v[3]);
+            else store4(a + col, v[0], v[1], v[2], v[3]);
+          }
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = mw + 32 * i + l32;

@@ -20,7 +20,7 @@ STATUS = {0: "LCE_OK", 1: "LCE_ERR_INVALID_ARGUMENT", 2: "LCE_ERR_UNSUPPORTED",
           3: "LCE_ERR_WORKSPACE_TOO_SMALL", 4: "LCE_ERR_HIP"}
 DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
-EXPORTED = ("lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
+EXPORTED = ("lce_workspace_size", "lce_plan_info", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
             "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward", "lce_rmsnorm_forward_backward",
             "lce_host_adam_step", "lce_head_train_step",
             "lce_timing_enable", "lce_timing_read", "lce_status_string")
@@ -36,6 +36,17 @@ class HeadStepTiming(ctypes.Structure):
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class PlanInfo(ctypes.Structure):
+    """lce_plan_info_t."""
+    _fields_ = [("chunk_tokens", ctypes.c_int64), ("chunks", ctypes.c_int64), ("dh_splits", ctypes.c_int32),
+                ("target_referenced", ctypes.c_int32), ("dw_fp32_carry", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("workspace_bytes", ctypes.c_size_t),
+                ("fallback_flags_offset", ctypes.c_size_t)]
+
+    def as_dict(self):
+        return {k: int(getattr(self, k)) for k, _ in self._fields_ if k != "reserved"}
 
 
 class AdamConfig(ctypes.Structure):
@@ -61,6 +72,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
     lib.lce_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, ctypes.c_int, i64]
     lib.lce_workspace_size.restype = sz
+    lib.lce_plan_info.argtypes = [i64, i64, i64, ctypes.c_int, ctypes.c_int, i64, ctypes.POINTER(PlanInfo)]
+    lib.lce_plan_info.restype = ctypes.c_int
     lib.lce_auto_chunk_tokens.argtypes = [i64, i64, i64, ctypes.c_int]
     lib.lce_auto_chunk_tokens.restype = i64
     lib.lce_forward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp, sz, vp]
@@ -137,6 +150,16 @@ def _check_inputs(hidden, weight, labels):
 def workspace_size(N: int, H: int, V: int, dtype=torch.bfloat16, with_backward: bool = True,
                    chunk_tokens: int = 0) -> int:
     return int(load_library().lce_workspace_size(N, H, V, DTYPES[dtype], int(with_backward), chunk_tokens))
+
+
+def plan_info(N: int, H: int, V: int, dtype=torch.bfloat16, with_backward: bool = True,
+              chunk_tokens: int = 0) -> dict:
+    """How a call with these sizes runs (lce_plan_info): chunking, dH splits, dW carry, flags offset."""
+    info = PlanInfo()
+    st = load_library().lce_plan_info(N, H, V, DTYPES[dtype], int(with_backward), chunk_tokens, ctypes.byref(info))
+    if st != LCE_OK:
+        raise LCEError(st, "lce_plan_info")
+    return info.as_dict()
 
 
 def auto_chunk_tokens(N: int, H: int, V: int, dtype=torch.bfloat16) -> int:

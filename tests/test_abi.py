@@ -30,7 +30,7 @@ def _declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
-    assert names == sorted(["lce_workspace_size", "lce_auto_chunk_tokens", "lce_forward",
+    assert names == sorted(["lce_workspace_size", "lce_plan_info", "lce_auto_chunk_tokens", "lce_forward",
                             "lce_forward_backward", "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward",
                             "lce_rmsnorm_forward_backward", "lce_host_adam_step", "lce_head_train_step",
                             "lce_timing_enable",
@@ -73,7 +73,10 @@ def test_workspace_size(lib):
     b = ws(16384, 4096, 128256, BF16, 1, 4096)
     assert 0 < b - a <= 8192 * 4096 * 2 + 8192 * 64
     assert lib.lce_auto_chunk_tokens(8192, 4096, 128256, BF16) == 4096
-    assert lib.lce_auto_chunk_tokens(16384, 3584, 152064, BF16) == 3584
+    # Qwen: min(H, N/2) = 3584 would give five chunks, above bf16's carry limit of four; four chunks
+    # of 4096 cost 156 MB more e buffer instead of a 2.18 GB fp32 accumulator. fp16's limit is 9.
+    assert lib.lce_auto_chunk_tokens(16384, 3584, 152064, BF16) == 4096
+    assert lib.lce_auto_chunk_tokens(16384, 3584, 152064, FP16) == 3584
     assert lib.lce_auto_chunk_tokens(4096, 12288, 32768, BF16) == 2048
     assert lib.lce_auto_chunk_tokens(37, 72, 1000, BF16) == 37  # one chunk
     # Forward only: one chunk up to 16384 tokens (per-slice partials, no logits-shaped buffer).
@@ -204,3 +207,57 @@ def test_head_train_step_rejects_bad_optimizer_settings(lib):
     for cfg in (L.AdamConfig(-1e-3, 0.9, 0.999, 1e-8, 0.0), L.AdamConfig(1e-3, 1.0, 0.999, 1e-8, 0.0),
                 L.AdamConfig(1e-3, 0.9, 0.999, 0.0, 0.0), L.AdamConfig(1e-3, 0.9, 0.999, 1e-8, -0.5)):
         assert _head(lib, cfg=cfg) == INVALID
+
+
+def test_gpu_parity_cases_cover_every_path():
+    """The whole-oracle GPU parity cases (tests/test_gpu_parity.py) reach every way the backward can
+    run, by the library's own plan: for each dtype, a dH contraction that stores its rows directly
+    (one chunk, and several with dW added to across chunks) and one split over the vocabulary;
+    for the 16-bit types, dW carried across chunks in fp32; and a chunk count at each carry limit."""
+    import test_gpu_parity as gp
+    from paper_2603_16428_amd import lce
+    import torch
+    dt = {"bf16": torch.bfloat16, "fp16": torch.float16, "fp32": torch.float32}
+    cases = [(N, H, V, d, c) for N, H, V, d, c in gp.RAGGED + gp.NAN_WS]
+    cases += [(N, H, V, d, c) for N, H, V, d, c, _ in gp.UNSPLIT]
+    cases += [(16384, 4096, 4096, "bf16", c) for c in (4096, 1024, 0)]   # test_many_chunks_llama_width
+    cases += [(4096, 1024, 4096, "fp16", c) for c in (512, 256)]         # test_many_chunks_fp16
+    seen = set()
+    for N, H, V, d, c in cases:
+        p = lce.plan_info(N, H, V, dt[d], True, c)
+        seen.add((d, "unsplit" if p["dh_splits"] == 1 else "split", "1 chunk" if p["chunks"] == 1 else "chunks",
+                  "fp32 carry" if p["dw_fp32_carry"] else "own carry"))
+    for d in ("bf16", "fp16", "fp32"):
+        assert (d, "unsplit", "1 chunk", "own carry") in seen, d
+        assert (d, "unsplit", "chunks", "own carry") in seen, d
+        assert (d, "split", "chunks", "own carry") in seen, d
+    for d in ("bf16", "fp16"):
+        assert any(k[0] == d and k[3] == "fp32 carry" for k in seen), d
+    # The full-size workloads run unsplit (Llama, Qwen) and split (Mistral-Large).
+    assert lce.plan_info(8192, 4096, 128256, torch.bfloat16)["dh_splits"] == 1
+    assert lce.plan_info(16384, 3584, 152064, torch.bfloat16)["dh_splits"] == 1
+    assert lce.plan_info(4096, 12288, 32768, torch.bfloat16)["dh_splits"] > 1
+
+
+def test_plan_info(lib):
+    from paper_2603_16428_amd import lce
+    info = lce.PlanInfo()
+    assert lib.lce_plan_info(8, 8, 8, BF16, 1, 0, None) == INVALID
+    assert lib.lce_plan_info(0, 8, 8, BF16, 1, 0, ctypes.byref(info)) == INVALID
+    assert lib.lce_plan_info(8, 12, 8, BF16, 1, 0, ctypes.byref(info)) == UNSUPPORTED
+    for args in [(8192, 4096, 128256, BF16, 1, 0), (8192, 4096, 128256, BF16, 0, 0), (300, 136, 4099, FP32, 1, 64),
+                 (16384, 4096, 4096, BF16, 1, 1024), (65536, 4096, 128256, FP16, 1, 0)]:
+        assert lib.lce_plan_info(*args, ctypes.byref(info)) == OK
+        assert info.workspace_bytes == lib.lce_workspace_size(*args)
+        assert info.chunks == -(-args[0] // info.chunk_tokens)
+        if args[4]:
+            assert info.chunk_tokens == (args[5] or lib.lce_auto_chunk_tokens(*args[:4]))
+            assert 0 < info.fallback_flags_offset and info.fallback_flags_offset + 4 * info.chunks <= info.workspace_bytes
+        else:
+            assert info.dh_splits == 0 and info.fallback_flags_offset == 0
+    # The fp32 carry costs V x H fp32 of workspace.
+    assert lib.lce_plan_info(16384, 4096, 4096, BF16, 1, 1024, ctypes.byref(info)) == OK and info.dw_fp32_carry == 1
+    with_acc = info.workspace_bytes
+    assert lib.lce_plan_info(16384, 4096, 4096, BF16, 1, 4096, ctypes.byref(info)) == OK and info.dw_fp32_carry == 0
+    assert lib.lce_workspace_size(16384, 4096, 4096, FP32, 1, 1024) > 0
+    assert with_acc - lib.lce_workspace_size(16384, 4096, 4096, BF16, 1, 4096) >= 4096 * 4096 * 4 - 3 * 1024 * 4096 * 2

@@ -49,6 +49,22 @@ def test_pipelined_equals_sequential(lce, N, H, V, dtype, chunk, blocks):
     assert torch.equal(a.weight, b.weight) and torch.equal(a.grad_weight, b.grad_weight)
 
 
+# The last chunk's dW contraction in vocabulary blocks gives the same dW, bit for bit, as the plain
+# step's single launch: with dW carried across chunks in its own type (2 chunks) and in the fp32
+# accumulator (8 chunks, above bf16's carry limit of 4).
+@pytest.mark.parametrize("chunk,carry", [(512, 0), (128, 1)])
+def test_blocked_dw_equals_plain_step(lce, chunk, carry):
+    N, H, V = 1024, 256, 9000
+    d, X, y = _case(N, H, V, "bf16", seed=17)
+    assert lce.plan_info(N, H, V, torch.bfloat16, True, chunk)["dw_fp32_carry"] == carry
+    W = d["weight"].cuda()
+    loss, dH, dW = lce.forward_backward(X, W, y, chunk_tokens=chunk)
+    st = _state(lce, d)
+    l2, dH2, _ = lce.head_train_step(st, X, y, chunk_tokens=chunk, vocab_blocks=6, **ADAM)
+    torch.cuda.synchronize()
+    assert torch.equal(loss, l2) and torch.equal(dH, dH2) and torch.equal(dW, st.grad_weight)
+
+
 def test_buffers_and_first_update_against_oracle(lce):
     N, H, V = 400, 192, 5000
     d, X, y = _case(N, H, V, "bf16", seed=11)
