@@ -149,6 +149,29 @@ lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* 
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * lce_forward without a workspace argument and without allocating, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. Same arguments, results and errors as lce_forward, except:
+ *   - Scratch is a static device array of LCE_NO_ALLOC_SCRATCH_BYTES (64 MiB) inside the library,
+ *     one per device, held from the library's first use on that device until the process ends.
+ *     The call picks the largest chunk of tokens whose workspace fits it (the results do not depend
+ *     on the chunk) and returns LCE_ERR_WORKSPACE_TOO_SMALL, before anything is enqueued, when even
+ *     64 tokens per chunk need more (the per-token part is 12 N bytes: N up to about 5 million at
+ *     H = 4096, V = 128256).
+ *   - The array is shared by every call on a device and keeps the last call's contents (nothing in
+ *     it has to start at zero). Calls that overlap on one device -- on different streams, or from
+ *     different threads without ordering -- race on it: the caller orders them (one stream, or
+ *     events). `stream` must belong to the current device.
+ *   - The first call on a device looks up the array's address (hipGetSymbolAddress); no call
+ *     allocates or frees memory (no hipMalloc, hipFree or allocating library routine).
+ */
+#define LCE_NO_ALLOC_SCRATCH_BYTES (64u << 20)
+lce_status_t lce_forward_no_alloc(const void* hidden, const void* weight, const int64_t* labels,
+                                  int64_t N, int64_t H, int64_t V, int dtype,
+                                  int64_t ignore_index, int reduction,
+                                  float* loss, float* lse, void* stream);
+
+/*
  * Forward and backward: the reduced loss and its gradients with respect to hidden and weight
  * (upstream gradient 1; scale both outputs for another upstream value). This is the fused step of
  * Section 3.3 (paragraph "Optimized Triton Kernels"): the gradients are produced token chunk by

@@ -25,6 +25,12 @@
 #include "lce_aux.hpp"
 #include "lce_gemm.hpp"
 
+// Scratch memory of lce_forward_no_alloc: the workspace of a forward call, in a static device array
+// that every device the library runs on holds (its own copy, at its own address) until the process
+// ends. Host code never passes this name to a kernel: the name is a host-side stand-in, and the
+// device address comes from hipGetSymbolAddress (lce::no_alloc_scratch below).
+static __device__ __align__(256) char scratch[LCE_NO_ALLOC_SCRATCH_BYTES];
+
 namespace lce {
 namespace {
 
@@ -71,6 +77,25 @@ class KernelTimer {
   bool active_ = false;
 };
 int64_t cdiv(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+// The device address of `scratch` on the current device, looked up on the first call per device
+// (with that device current) and kept.
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+lce_status_t no_alloc_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return LCE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return LCE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return LCE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LCE_OK;
+}
 
 struct Plan {
   int64_t N = 0, H = 0, V = 0;
@@ -231,6 +256,29 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   }
   p.total = off;
   return LCE_OK;
+}
+
+// The forward plan of lce_forward_no_alloc: the automatic chunk if it is valid and its workspace
+// fits the static scratch, else the largest multiple of 64 tokens below it that is and does (both
+// the workspace and the 32-bit limits of make_plan grow with the chunk, so a binary search finds
+// it). An error at 64 tokens per chunk does not depend on the chunk and is returned as it is;
+// LCE_ERR_WORKSPACE_TOO_SMALL when 64 tokens per chunk are valid but do not fit.
+lce_status_t make_no_alloc_plan(int64_t N, int64_t H, int64_t V, int dtype, Plan& p) {
+  const size_t cap = (size_t)LCE_NO_ALLOC_SCRATCH_BYTES;
+  lce_status_t st = make_plan(N, H, V, dtype, false, 0, p, true);
+  if (st == LCE_OK && p.total <= cap) return LCE_OK;
+  const int64_t top = st == LCE_OK ? p.nc : N;
+  Plan q;
+  st = make_plan(N, H, V, dtype, false, 64, q, true);
+  if (st != LCE_OK) return st;
+  if (q.total > cap) return LCE_ERR_WORKSPACE_TOO_SMALL;
+  int64_t lo = 1, hi = (top - 1) / 64;  // chunks of 64 lo tokens are valid and fit
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) / 2;
+    if (make_plan(N, H, V, dtype, false, mid * 64, q, true) == LCE_OK && q.total <= cap) lo = mid;
+    else hi = mid - 1;
+  }
+  return make_plan(N, H, V, dtype, false, lo * 64, p, true);
 }
 
 // AL: operand A's layout (ALayout); operand B is blocked. KCHECK: a K-contig A's K range may end
@@ -698,6 +746,29 @@ lce_status_t lce_forward(const void* hidden, const void* weight, const int64_t* 
                               reduction, loss, lse, nullptr, nullptr, (char*)workspace, s);
   return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss, lse,
                          nullptr, nullptr, (char*)workspace, s);
+}
+
+lce_status_t lce_forward_no_alloc(const void* hidden, const void* weight, const int64_t* labels, int64_t N,
+                                  int64_t H, int64_t V, int dtype, int64_t ignore_index, int reduction, float* loss,
+                                  float* lse, void* stream) {
+  if (!hidden || !weight || !labels || !loss) return LCE_ERR_INVALID_ARGUMENT;
+  if (reduction != LCE_REDUCTION_NONE && reduction != LCE_REDUCTION_MEAN && reduction != LCE_REDUCTION_SUM)
+    return LCE_ERR_INVALID_ARGUMENT;
+  lce::Plan p;
+  lce_status_t st = lce::make_no_alloc_plan(N, H, V, dtype, p);
+  if (st != LCE_OK) return st;
+  void* ws = nullptr;
+  st = lce::no_alloc_scratch(&ws);
+  if (st != LCE_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LCE_DTYPE_BF16)
+    return lce::run<lce::bf16>(p, (const lce::bf16*)hidden, (const lce::bf16*)weight, labels, ignore_index,
+                               reduction, loss, lse, nullptr, nullptr, (char*)ws, s);
+  if (dtype == LCE_DTYPE_FP16)
+    return lce::run<lce::f16>(p, (const lce::f16*)hidden, (const lce::f16*)weight, labels, ignore_index,
+                              reduction, loss, lse, nullptr, nullptr, (char*)ws, s);
+  return lce::run<float>(p, (const float*)hidden, (const float*)weight, labels, ignore_index, reduction, loss, lse,
+                         nullptr, nullptr, (char*)ws, s);
 }
 
 lce_status_t lce_forward_backward(const void* hidden, const void* weight, const int64_t* labels, int64_t N,

@@ -20,7 +20,8 @@ STATUS = {0: "LCE_OK", 1: "LCE_ERR_INVALID_ARGUMENT", 2: "LCE_ERR_UNSUPPORTED",
           3: "LCE_ERR_WORKSPACE_TOO_SMALL", 4: "LCE_ERR_HIP"}
 DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 REDUCTIONS = {"none": 0, "mean": 1, "sum": 2}
-EXPORTED = ("lce_workspace_size", "lce_plan_info", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_backward",
+EXPORTED = ("lce_workspace_size", "lce_plan_info", "lce_auto_chunk_tokens", "lce_forward", "lce_forward_no_alloc",
+            "lce_forward_backward",
             "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward", "lce_rmsnorm_forward_backward",
             "lce_host_adam_step", "lce_head_train_step",
             "lce_timing_enable", "lce_timing_read", "lce_status_string")
@@ -78,6 +79,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.lce_auto_chunk_tokens.restype = i64
     lib.lce_forward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp, sz, vp]
     lib.lce_forward.restype = ctypes.c_int
+    lib.lce_forward_no_alloc.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp]
+    lib.lce_forward_no_alloc.restype = ctypes.c_int
     lib.lce_forward_backward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, i64, ctypes.c_int, vp, vp, vp,
                                          i64, vp, sz, vp]
     lib.lce_forward_backward.restype = ctypes.c_int
@@ -190,6 +193,26 @@ def forward(hidden, weight, labels, ignore_index: int = -100, reduction: str = "
         raise LCEError(st, "lce_forward")
     loss = loss if red == 0 else loss[0]
     return (loss, lse) if return_lse else loss
+
+
+def forward_no_alloc(hidden, weight, labels, ignore_index: int = -100, reduction: str = "mean",
+                     return_lse: bool = False, loss=None, lse=None):
+    """forward() through lce_forward_no_alloc: the library uses its static scratch, no workspace.
+    `loss` / `lse` may be given (preallocated outputs) so that the call allocates nothing at all."""
+    lib = load_library()
+    N, H, V = _check_inputs(hidden, weight, labels)
+    red = REDUCTIONS[reduction]
+    if loss is None:
+        loss = torch.empty(N if red == 0 else 1, dtype=torch.float32, device=hidden.device)
+    if return_lse and lse is None:
+        lse = torch.empty(N, dtype=torch.float32, device=hidden.device)
+    stream = ctypes.c_void_p(torch.cuda.current_stream(hidden.device).cuda_stream)
+    st = lib.lce_forward_no_alloc(_ptr(hidden), _ptr(weight), _ptr(labels), N, H, V, DTYPES[hidden.dtype],
+                                  ignore_index, red, _ptr(loss), _ptr(lse if return_lse else None), stream)
+    if st != LCE_OK:
+        raise LCEError(st, "lce_forward_no_alloc")
+    out = loss if red == 0 else loss[0]
+    return (out, lse) if return_lse else out
 
 
 def forward_backward(hidden, weight, labels, ignore_index: int = -100, reduction: str = "mean",

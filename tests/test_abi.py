@@ -31,6 +31,7 @@ def _declared_functions():
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lce_workspace_size", "lce_plan_info", "lce_auto_chunk_tokens", "lce_forward",
+                            "lce_forward_no_alloc",
                             "lce_forward_backward", "lce_rmsnorm_workspace_size", "lce_rmsnorm_forward",
                             "lce_rmsnorm_forward_backward", "lce_host_adam_step", "lce_head_train_step",
                             "lce_timing_enable",
@@ -261,3 +262,14 @@ def test_plan_info(lib):
     assert lib.lce_plan_info(16384, 4096, 4096, BF16, 1, 4096, ctypes.byref(info)) == OK and info.dw_fp32_carry == 0
     assert lib.lce_workspace_size(16384, 4096, 4096, FP32, 1, 1024) > 0
     assert with_acc - lib.lce_workspace_size(16384, 4096, 4096, BF16, 1, 4096) >= 4096 * 4096 * 4 - 3 * 1024 * 4096 * 2
+
+
+def test_no_alloc_forward_rejects_before_launching(lib):
+    # Invalid arguments as for lce_forward; sizes whose workspace cannot fit the static scratch even
+    # at 64 tokens per chunk: LCE_ERR_WORKSPACE_TOO_SMALL, decided on the host before any HIP call.
+    f = lib.lce_forward_no_alloc
+    assert f(None, FAKE, FAKE, 8, 8, 8, BF16, -100, MEAN, FAKE, None, None) == INVALID
+    assert f(FAKE, FAKE, FAKE, 8, 8, 8, BF16, -100, 7, FAKE, None, None) == INVALID
+    assert f(FAKE, FAKE, FAKE, 8, 12, 8, BF16, -100, MEAN, FAKE, None, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, 8 << 20, 4096, 128256, BF16, -100, MEAN, FAKE, None, None) == WS_SMALL
+    assert f(FAKE, FAKE, FAKE, 4096, 1 << 20, 256, BF16, -100, MEAN, FAKE, None, None) == WS_SMALL
