@@ -749,7 +749,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     const float sc = dz_epilogue_scale<T>(g.n_valid, g.mean);
     if (g.mode >= DW_ACC32_FIRST) {
       // fp32 cross-chunk accumulator: acc32 (+)= sc * C, or at the last chunk dW = acc32 + sc * C
-      // rounded once. A row's sixteen 16-byte pieces are requested together before any is used.
+      // rounded once. A block's four 16-byte pieces are requested together before any is used.
       const bool read = g.mode != DW_ACC32_FIRST, last = g.mode == DW_ACC32_LAST;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -757,25 +757,24 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
         if (row >= g.M) continue;
         float* a = g.acc32 + (size_t)row * g.ldo;
         T* o = (T*)g.out + (size_t)row * g.ldo;
-        f32x4 base[4][4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j) {
+          f32x4 base[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int col = nw + 32 * j + 8 * q + sub4;
-            base[j][q] = (read && col < g.N) ? *(const f32x4*)(a + col) : (f32x4){};
+            base[q] = (read && col < g.N) ? *(const f32x4*)(a + col) : (f32x4){};
           }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int col = nw + 32 * j + 8 * q + sub4;
             if (col >= g.N) continue;
-            const f32x4 v = base[j][q] + sc * (f32x4){acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                                      acc[i][j][4 * q + 3]};
+            const f32x4 v = base[q] + sc * (f32x4){acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                                   acc[i][j][4 * q + 3]};
             if (last) store4(o + col, v[0], v[1], v[2], v[3]);
             else store4(a + col, v[0], v[1], v[2], v[3]);
           }
+        }
       }
       return;
     }
