@@ -176,24 +176,51 @@ def other_workload(lce, name, dtype_override, steps=10, warmup=3):
     for _ in range(warmup):
         lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
     torch.cuda.synchronize()
-    lce.timing_enable(True)
     stream = torch.cuda.current_stream()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # The step time without per-kernel events (a short step's host work would show in it), then
+    # the same steps again with them, for each kernel kind's share.
     a.record(stream)
     for _ in range(steps):
         lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
     b.record(stream)
     torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    lce.timing_enable(True)
+    for _ in range(steps):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
+    torch.cuda.synchronize()
     kern = lce.timing_read()
     lce.timing_enable(False)
-    ms = a.elapsed_time(b) / steps
     peak = PEAK_FP32_TFLOPS if X.dtype == torch.float32 else PEAK_BF16_TFLOPS
     frac = 6.0 * N * H * V / (ms * 1e-3) / 1e12 / peak
+    # The same step replayed from a HIP graph.
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    cg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(cg):
+        lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], 0, ws, out)
+    for _ in range(warmup):
+        cg.replay()
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(steps):
+        cg.replay()
+    b.record(stream)
+    torch.cuda.synchronize()
+    gms = a.elapsed_time(b) / steps
+    del cg
     rec = {"N": N, "H": H, "V": V, "dtype": d["dtype"], "reduction": d["reduction"], "steps": steps,
            "chunk_tokens": plan["chunk_tokens"], "chunks": plan["chunks"], "dh_splits": plan["dh_splits"],
            "ms_per_step": round(ms, 4), "tokens_per_s": round(N / (ms * 1e-3), 1), "mfma_peak_frac": round(frac, 4),
+           "graph_replay_ms_per_step": round(gms, 4),
            "kernels_ms_per_step": {k: round(v[0] / steps, 4) for k, v in kern.items() if v[1]}}
-    log(f"{name}: {ms:.3f} ms/step ({100 * frac:.1f}% of peak; inputs {time.time() - t0:.0f} s)")
+    log(f"{name}: {ms:.3f} ms/step ({100 * frac:.1f}% of peak), graph replay {gms:.3f} ms/step; "
+        f"inputs {time.time() - t0:.0f} s")
     del X, W, y, ws, out
     torch.cuda.empty_cache()
     return rec
@@ -215,6 +242,7 @@ def main():
     ap.add_argument("--no-memory", action="store_true", help="skip the materialised-logits comparison")
     ap.add_argument("--no-rmsnorm", action="store_true", help="skip timing the variant with the final RMSNorm")
     ap.add_argument("--no-blas", action="store_true", help="skip the hipBLASLt GEMMs timed as context")
+    ap.add_argument("--no-graph", action="store_true", help="skip timing the step replayed from a HIP graph")
     ap.add_argument("--no-head-train", action="store_true",
                     help="skip the output-layer training step with host-resident weights")
     ap.add_argument("--vocab-blocks", type=int, default=8, help="pipeline blocks of the head training step")
@@ -308,6 +336,34 @@ def main():
     w_stream.update({"unit": "GB/s", "w_bytes_per_launch": w_bytes, "launches_per_step": chunks,
                      "hbm_peak_gbs": PEAK_HBM_GBS})
     log("W streams: " + ", ".join(f"{k} {v}" for k, v in w_stream.items()))
+
+    # The same step captured once in a HIP graph and replayed (the library allocates nothing and
+    # never synchronizes, so a caller can capture it): no host launch work per kernel.
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        cg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(cg):
+            lce.forward_backward(X, W, y, d["ignore_index"], d["reduction"], args.chunk, ws, out)
+        for _ in range(args.warmup):
+            cg.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(args.steps):
+            cg.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        gms = g0.elapsed_time(g1) / args.steps
+        graph = {"ms_per_step": round(gms, 4), "tokens_per_s": round(N / (gms * 1e-3), 1),
+                 "mfma_peak_frac": round(flops / (gms * 1e-3) / 1e12 / peak, 4)}
+        del cg
+        log(f"graph replay: {gms:.3f} ms/step")
 
     # Context: the three contraction shapes of one chunk as plain hipBLASLt GEMMs (torch.mm, 2-D
     # operands; no epilogue work, no log-sum-exp, no dlogits).
@@ -424,7 +480,8 @@ def main():
         "config": {"workload": wl_name,
                    "N": N, "H": H, "V": V, "reduction": d["reduction"],
                    "chunk_tokens": chunk, "chunks": chunks, "seed": 0},
-        "roofline": roofline, "w_stream": w_stream, "forward_only": forward_only, "rmsnorm_fused": rmsnorm,
+        "roofline": roofline, "w_stream": w_stream, "graph_replay": graph, "forward_only": forward_only,
+        "rmsnorm_fused": rmsnorm,
         "head_train_step": head, "memory": memory, "hipblaslt_context": blas,
     }
     others = [w for w in args.other_workloads.split(",") if w]

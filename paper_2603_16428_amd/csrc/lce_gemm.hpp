@@ -617,86 +617,84 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     if (mw >= g.M) return;
     const int slice = mw / kLseSlice;
     const bool tref = EPI == EPI_LSE_BWD && g.ref != nullptr;
+    // Each logit costs a few VALU instructions and an exponential here. Only the last tile row has
+    // rows at or beyond M; every other wave runs the body without the per-value bound check (a
+    // uniform branch), and each block's exponentials go from VGPRs straight to the e' store
+    // instead of back through the accumulator registers.
+    auto body = [&](auto full_c) {
+      constexpr bool FULL = decltype(full_c)::value;
+      auto inside = [&](int i, int r) { return FULL || mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3) < g.M; };
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = nw + 32 * j + l32;
-      const bool in = col < g.N;
-      float m_ref, s = 0.f;
-      if (tref) {
-        // Target-referenced: the token's reference (the tile's references were copied to LDS while
-        // the pipeline filled). A token without one (ignored, invalid label, padding) takes +inf,
-        // so its e is exactly 0 and its partial sum 0: a backward call reports no lse, and such a
-        // token's loss does not depend on it.
-        const float ref = *(const float*)(refs_lds + 4 * (col - n0));
-        const bool keep = in && __builtin_isfinite(ref);
-        m_ref = keep ? ref : 0.f;
-        const float ml = keep ? ref * kLog2e : INFINITY;
+      for (int j = 0; j < 4; ++j) {
+        const int col = nw + 32 * j + l32;
+        const bool in = col < g.N;
+        float m_ref, ml, s = 0.f;
+        if (tref) {
+          // Target-referenced: the token's reference (the tile's references were copied to LDS
+          // while the pipeline filled). A token without one (ignored, invalid label, padding) takes
+          // +inf, so its e is exactly 0 and its partial sum 0: a backward call reports no lse, and
+          // such a token's loss does not depend on it.
+          const float ref = *(const float*)(refs_lds + 4 * (col - n0));
+          const bool keep = in && __builtin_isfinite(ref);
+          m_ref = keep ? ref : 0.f;
+          ml = keep ? ref * kLog2e : INFINITY;
+        } else {
+          // The slice maximum as the reference.
+          float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-            const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
-            s += e;
-            acc[i][j][r] = e;
-          }
-      } else {
-        // The slice maximum as the reference.
-        float mx = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-            if (row < g.M) mx = fmaxf(mx, acc[i][j][r]);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        m_ref = mx;
-        const float ml = mx * kLog2e;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = mw + 32 * i + 8 * (r >> 2) + sub4 + (r & 3);
-            const float e = row < g.M ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
-            s += e;
-            acc[i][j][r] = e * Storage<T>::kE;
-          }
-      }
-      s += __shfl_xor(s, 32);
-      if constexpr (EPI == EPI_LSE_BWD) {
+            for (int r = 0; r < 16; ++r)
+              if (inside(i, r)) mx = fmaxf(mx, acc[i][j][r]);
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          m_ref = mx;
+          ml = mx * kLog2e;
+        }
         // Every token block that holds a token of the chunk is written whole: target-referenced,
         // the lanes of tokens at or beyond N store zeros (the dW GEMM sums over the last block).
-        if (nw + 32 * j < g.N) {
-          // e blocked: the token is column l%32 of token block col/32, so this lane's piece of every
-          // fragment of that block is at lane * 16; 32 ids fill the lane's pieces of two fragments.
-          char* e_blk = (char*)g.out + (size_t)((nw + 32 * j) >> 5) * g.ldo * 1024 + lane * 16;
-          if constexpr (kEsz == 2) {
-            // Whole 128-row wave slices: the blocked rows cover M rounded up to 256, and rows at or
-            // beyond M hold exp = 0 here.
+        // e blocked: the token is column l%32 of token block col/32, so this lane's piece of every
+        // fragment of that block is at lane * 16; 32 ids fill the lane's pieces of two fragments.
+        const bool store = EPI == EPI_LSE_BWD && nw + 32 * j < g.N;
+        char* e_blk = (char*)g.out + (size_t)((nw + 32 * j) >> 5) * g.ldo * 1024 + lane * 16;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) store_frag32<T>(e_blk + (size_t)((mw + 32 * i) >> 4) * 1024, acc[i][j]);
-          } else {
-            // fp32: a K-pair is 8 ids, half of it per lane half. The dH GEMM reads every K-pair that
-            // holds an id below M whole, so such a K-pair is stored whole: its ids at or beyond M
-            // hold exp = 0 here, and nothing stale from the workspace reaches the contraction.
+        for (int i = 0; i < 4; ++i) {
+          f32x16 ev;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+          for (int r = 0; r < 16; ++r) {
+            const float e = inside(i, r) ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -ml)) : 0.f;
+            s += e;
+            ev[r] = e * Storage<T>::kE;
+          }
+          if constexpr (EPI == EPI_LSE_BWD) {
+            if (store) {
+              if constexpr (kEsz == 2) {
+                // Whole 128-row wave slices: the blocked rows cover M rounded up to 256, and rows
+                // at or beyond M hold exp = 0 here.
+                store_frag32<T>(e_blk + (size_t)((mw + 32 * i) >> 4) * 1024, ev);
+              } else {
+                // fp32: a K-pair is 8 ids, half of it per lane half. The dH GEMM reads every K-pair
+                // that holds an id below M whole, so such a K-pair is stored whole: its ids at or
+                // beyond M hold exp = 0 here, and nothing stale from the workspace reaches it.
 #pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const int kp_row = mw + 32 * i + 8 * q;
-                if (kp_row < g.M)
-                  store4((T*)(e_blk + (size_t)(kp_row >> 3) * 1024), acc[i][j][4 * q],
-                         acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                for (int q = 0; q < 4; ++q) {
+                  const int kp_row = mw + 32 * i + 8 * q;
+                  if (FULL || kp_row < g.M)
+                    store4((T*)(e_blk + (size_t)(kp_row >> 3) * 1024), ev[4 * q], ev[4 * q + 1], ev[4 * q + 2],
+                           ev[4 * q + 3]);
+                }
               }
+            }
           }
         }
+        s += __shfl_xor(s, 32);
+        if (in && lane < 32) {
+          g.pmax[(size_t)slice * g.ldp + col] = m_ref;
+          g.psum[(size_t)slice * g.ldp + col] = s;
+        }
       }
-      if (in && lane < 32) {
-        g.pmax[(size_t)slice * g.ldp + col] = m_ref;
-        g.psum[(size_t)slice * g.ldp + col] = s;
-      }
-    }
+    };
+    if (mw + 128 <= g.M) body(std::true_type{});
+    else body(std::false_type{});
   } else if constexpr (EPI == EPI_STORE) {
     // C^T token-major: column n = nw + 32j + l%32 of C is row n of the output, and the lane's four
     // consecutive rows of C per (i, q) are four consecutive elements of it. M (the output's row
