@@ -279,8 +279,9 @@ lce_status_t lce_host_adam_step(float* param, const void* grad, int dtype, float
  *   step        : Adam step count (>= 1); vocab_blocks in [1, 256].
  *   timing      : optional; receives the phases of this call (milliseconds).
  * Unlike the other entry points this call synchronises: it returns when the update and the copies
- * are complete (and `stream` is ordered after them). It creates and destroys two non-blocking
- * streams and its events per call; it allocates no memory. Errors as for lce_forward_backward and
+ * are complete (and `stream` is ordered after them). Its two side streams (non-blocking, default
+ * priority) are created on the first call on a device and kept until the process ends; calls on one
+ * device share them. It creates and destroys its events per call and allocates no memory. Errors as for lce_forward_backward and
  * lce_host_adam_step; LCE_ERR_HIP if a copy or stream operation fails.
  */
 typedef struct {

@@ -575,6 +575,28 @@ lce_status_t run_rms(const RmsPlan& rp, const T* h, const T* gamma, const T* W, 
 // alone the pieces are blocks of vocabulary rows: the last chunk's dW GEMM runs block by block, each
 // block's gradient is copied out as soon as it is done, the host updates it while later blocks are
 // still being computed or copied, and the updated block is copied back on a second side stream.
+// The step's two side streams (gradient copies out, parameter copies in), one pair per device,
+// created (default priority, non-blocking) on the first call on that device and kept until the
+// process ends; calls on one device share them.
+std::mutex g_side_mu;
+hipStream_t g_side_d2h[kMaxDevices] = {}, g_side_h2d[kMaxDevices] = {};
+
+lce_status_t side_streams(hipStream_t& sd, hipStream_t& su) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return LCE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return LCE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_side_mu);
+  for (hipStream_t* p : {&g_side_d2h[dev], &g_side_h2d[dev]}) {
+    if (*p == nullptr && hipStreamCreateWithFlags(p, hipStreamNonBlocking) != hipSuccess) {
+      *p = nullptr;
+      return LCE_ERR_HIP;
+    }
+  }
+  sd = g_side_d2h[dev];
+  su = g_side_h2d[dev];
+  return LCE_OK;
+}
+
 struct StepClock {
   hipEvent_t a = nullptr, b = nullptr;
   bool ok() const { return a && b; }
@@ -607,8 +629,7 @@ lce_status_t run_head(const Plan& p, const T* X, const int64_t* y, int64_t ignor
   std::vector<int64_t> row0(blocks + 1, 0);
   hipEvent_t g0 = nullptr, g1 = nullptr, dh_done = nullptr, upd_end = nullptr;
   do {
-    if (hipStreamCreateWithFlags(&sd, hipStreamNonBlocking) != hipSuccess ||
-        hipStreamCreateWithFlags(&su, hipStreamNonBlocking) != hipSuccess) { st = LCE_ERR_HIP; break; }
+    if ((st = side_streams(sd, su)) != LCE_OK) break;
     g0 = ev(); g1 = ev(); dh_done = ev(); upd_end = ev();
     for (int b = 0; b < blocks; ++b) {
       dw_done[b] = ev(); d2h_a[b] = ev(); d2h_b[b] = ev(); h2d_a[b] = ev(); h2d_b[b] = ev();
@@ -688,8 +709,6 @@ lce_status_t run_head(const Plan& p, const T* X, const int64_t* y, int64_t ignor
     if (su) (void)hipStreamSynchronize(su);
   }
   for (auto e : evs) (void)hipEventDestroy(e);
-  if (sd) (void)hipStreamDestroy(sd);
-  if (su) (void)hipStreamDestroy(su);
   return st;
 }
 

@@ -107,6 +107,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const int t = threadIdx.x % kCombineTokens, grp = threadIdx.x / kCombineTokens;
   const int i = blockIdx.x * kCombineTokens + t;
   float m = -INFINITY, s = 0.f;
+  // Target-referenced partials all share one reference per token (its target logit, or 0 for a
+  // token without one), so the maxima are not read: the merge below runs with 0 in their place,
+  // where every factor exp(m - mn) is exactly 1 as it would be with the reference itself, and the
+  // reference is added back to the merged maximum.
+  const bool shared_ref = mode == CMB_TREF;
   if (i < rows) {
     // Eight slices' partials are requested before any is merged (the merge order is unchanged).
     constexpr int kAhead = 8;
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 #pragma unroll
       for (int u = 0; u < kAhead; ++u) {
         const int k = min(k0 + 16 * u, slices - 1);
-        mk[u] = pmax[(size_t)k * ldp + i];
+        mk[u] = shared_ref ? 0.f : pmax[(size_t)k * ldp + i];
         sk[u] = psum[(size_t)k * ldp + i];
       }
 #pragma unroll
@@ -135,8 +140,13 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     for (int k = 1; k < 16; ++k) M = fmaxf(M, sm[k][t]);
     float S = 0.f;
     for (int k = 0; k < 16; ++k) S += ss[k][t] * __expf(sm[k][t] - M);
-    const float lse = M + __logf(S);
     const int64_t lab = y[i];
+    if (shared_ref) {
+      // The logits epilogue's reference: the target logit of a valid token when finite, else 0.
+      const float r = tgt[i];
+      M = (lab != ignore_index && lab >= 0 && lab < V && __builtin_isfinite(r)) ? r : 0.f;
+    }
+    const float lse = M + __logf(S);
     lse_out[i] = lse;
     loss_out[i] = (lab == ignore_index) ? 0.f : lse - tgt[i];
     if (mode == CMB_TREF) {
