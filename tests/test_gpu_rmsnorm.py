@@ -73,6 +73,10 @@ CASES = [
     (129, 8, 300, "fp32", 0),
     (70, 520, 257, "bf16", 0),
     (1, 64, 128, "bf16", 0),
+    # Sixteen chunks: beyond the carry limits of bf16 (4) and fp16 (9), dW is summed over the chunks
+    # in the fp32 accumulator while dX comes out of the split dH partials in fp32.
+    (1024, 256, 3000, "bf16", 64),
+    (1024, 256, 3000, "fp16", 64),
 ]
 
 
