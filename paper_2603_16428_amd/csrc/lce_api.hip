@@ -209,9 +209,6 @@ lce_status_t make_plan(int64_t N, int64_t H, int64_t V, int dtype, bool backward
   if (p.xk_nb * p.xk_kp * 1024 > lim || p.xm_nb * p.xm_kp * 1024 > lim) return LCE_ERR_UNSUPPORTED;
   p.ez_nb = p.ncp / 32;
   p.ez_kp = round_up(V, kTile) * p.esz / 32;
-  // Grid y dimensions (at most 65535): block_mn_kernel's K-pair groups; a chunk's token blocks are
-  // held to the same bound.
-  if (p.ez_nb > 65535 || cdiv(p.xm_kp, 4) > 65535) return LCE_ERR_UNSUPPORTED;
 
   if (backward) {
     // dH tiles of one chunk: split the vocabulary (K) so that the grid fills the device.
@@ -338,32 +335,63 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
   float* acc32 = p.dw_acc32 ? (float*)(ws + p.o_acc32) : nullptr;
   const int mean = reduction == LCE_REDUCTION_MEAN;
 
+  // Small bandwidth-bound jobs share launches (aux_kernel): each launch boundary costs ~10 us of
+  // the step. The fragment-blocked copies of X_c: operand B of the logits GEMM (block_k) and,
+  // backward, of the dW GEMM (block_mn; target-referenced: scaled per token, so made once the
+  // factors are known).
+  auto bk_job = [&](AuxJobs& j, int64_t c) {
+    const int64_t t0 = c * p.nc;
+    j.bk_blocks = cdiv(p.xk_nb * p.xk_kp * 64, 256);
+    j.bk = BlockKJob{X + t0 * H, H, (int)std::min(p.nc, N - t0), (int)H, (int)p.xk_kp, (int)p.xk_nb, xk};
+  };
+  auto bmn_job = [&](AuxJobs& j, int64_t c, const float* row_scale) {
+    const int64_t t0 = c * p.nc;
+    j.bmn_blocks = p.xm_nb * cdiv(p.xm_kp, 4);
+    j.bmn = BlockMnJob{X + t0 * H, H, (int)H, (int)std::min(p.nc, N - t0), (int)p.xm_kp, (int)p.xm_nb, xm,
+                       row_scale};
+  };
+  auto dl_job = [&](AuxJobs& j, int64_t c, const int* run_if, int64_t blocks) {
+    const int64_t t0 = c * p.nc;
+    j.dl_blocks = blocks;
+    j.dl = DlogitsJob{ez, p.ez_kp, p.ez_nb, pmax, p.ncp, lse + t0, y + t0, ignore_index, nvalid, mean,
+                      (int)std::min(p.nc, N - t0), (int)V, run_if};
+  };
+  // The call's loss (reduction mean or sum): one block, in a launch after the last combine_kernel.
+  auto loss_job = [&](AuxJobs& j) {
+    if (reduction == LCE_REDUCTION_NONE) return;
+    j.loss_blocks = 1;
+    j.ls = LossJob{tl, N, nvalid, mean, loss};
+  };
+  auto aux = [&](const AuxJobs& j, TimingKind kind) {
+    KernelTimer t(kind, s);
+    const int64_t blocks = j.prep_blocks + j.bk_blocks + j.bmn_blocks + j.dl_blocks + j.loss_blocks;
+    hipLaunchKernelGGL((aux_kernel<T>), dim3((unsigned)blocks), dim3(256), 0, s, j);
+    return hipGetLastError();
+  };
   {
-    KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL((prepare_kernel<T>), dim3((unsigned)(cdiv(N, 4) + 1)), dim3(256), 0, s, X, W, y, N, H, V,
-                       ignore_index, tgt, tref, nvalid, flags, (int64_t)(flags ? p.chunks : 0));
+    // prepare (target logits, references, n_valid, flags) and chunk 0's copies.
+    AuxJobs j{};
+    j.prep_blocks = cdiv(N, 4) + 1;
+    j.prep = PrepareJob{X, W, y, N, H, V, ignore_index, tgt, tref, nvalid, flags, (int64_t)(flags ? p.chunks : 0)};
+    bk_job(j, 0);
+    if (p.backward && !p.tref) bmn_job(j, 0, nullptr);
+    if (aux(j, T_OTHER) != hipSuccess) return LCE_ERR_HIP;
   }
-  if (hipError_t e = hipGetLastError(); e != hipSuccess) return LCE_ERR_HIP;
+  bool bk_ready = true;  // X_c's block_k copy was made by an earlier launch
 
   for (int64_t c = 0; c < p.chunks; ++c) {
     const int64_t t0 = c * p.nc;
     const int rows = (int)std::min(p.nc, N - t0);
-
-    // Fragment-blocked copies of X_c: operand B of the logits GEMM and, backward, of the dW GEMM
-    // (target-referenced: scaled per token, so made once the factors are known).
-    auto block_x_for_dw = [&](const float* row_scale) {
-      KernelTimer t(T_OTHER, s);
-      hipLaunchKernelGGL((block_mn_kernel<T>), dim3((unsigned)p.xm_nb, (unsigned)cdiv(p.xm_kp, 4)), dim3(256), 0, s,
-                         X + t0 * H, H, (int)H, rows, (int)p.xm_kp, xm, row_scale);
-    };
-    {
-    KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL((block_k_kernel<T>), dim3((unsigned)cdiv(p.xk_nb * p.xk_kp * 64, 256)), dim3(256), 0, s,
-                       X + t0 * H, H, rows, (int)H, (int)p.xk_kp, (int)p.xk_nb, xk);
+    const bool last_chunk = c == p.chunks - 1;
+    // fp16 (not target-referenced): the unscaled dW operand copy, after the previous chunk's dW.
+    const bool bmn_now = c > 0 && p.backward && !p.tref;
+    if (!bk_ready || bmn_now) {
+      AuxJobs j{};
+      if (!bk_ready) bk_job(j, c);
+      if (bmn_now) bmn_job(j, c, nullptr);
+      if (aux(j, T_OTHER) != hipSuccess) return LCE_ERR_HIP;
     }
-    if (p.backward && !p.tref) block_x_for_dw(nullptr);
-    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
-
+    bk_ready = false;
     // logits^T tile = W . X_c^T with the log-sum-exp epilogue.
     GemmArgs g{};
     g.A = W; g.lda = H; g.M = (int)V;
@@ -393,20 +421,31 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
                          p.ncp, (int)p.slices, rows, y + t0, ignore_index, tgt + t0, lse + t0, tl + t0, mode,
                          scale ? scale + t0 : nullptr, (const int*)nvalid, mean, ez, p.ez_kp, V,
                          flags ? flags + c : nullptr, run_if);
+      return hipGetLastError();
     };
-    // dlogits, in place (blocked): a block per (K-pair group, token block), or a looped grid.
-    auto dlogits = [&](const int* run_if, int64_t grid) {
-      KernelTimer t(run_if ? T_OTHER : T_DLOGITS, s);
-      hipLaunchKernelGGL((dlogits_kernel<T>), dim3((unsigned)grid), dim3(256), 0, s, ez, p.ez_kp, p.ez_nb, pmax, p.ncp,
-                         lse + t0, y + t0, ignore_index, nvalid, mean, rows, (int)V, run_if);
-    };
-    combine(p.tref ? CMB_TREF : CMB_FORWARD, nullptr);
-    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
-    if (!p.backward) continue;
+    if (combine(p.tref ? CMB_TREF : CMB_FORWARD, nullptr) != hipSuccess) return LCE_ERR_HIP;
+    if (!p.backward) {
+      if (last_chunk) {
+        AuxJobs j{};
+        loss_job(j);
+        if (j.loss_blocks > 0 && aux(j, T_OTHER) != hipSuccess) return LCE_ERR_HIP;
+      }
+      continue;
+    }
 
+    // One launch after the chunk's combines: dlogits (in place, blocked), the dW operand's copy of
+    // X_c (target-referenced), and the next chunk's block_k copy (the logits GEMMs that read the
+    // current one have run) or, after the last chunk, the loss sum.
+    AuxJobs tail{};
+    if (!last_chunk) {
+      bk_job(tail, c + 1);
+      bk_ready = true;
+    } else {
+      loss_job(tail);
+    }
     if (p.tref) {
       // Only when combine flagged a token whose exp(z - z_target) may have overflowed: the chunk's
-      // logits again with slice-maximum references, combine, and dlogits (launches that return at
+      // logits again with slice-maximum references, combine, and dlogits (work that returns at
       // once when the flag is clear).
       const int* flag = flags + c;
       GemmArgs gf = g;
@@ -417,13 +456,15 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
       e = whole ? launch_gemm<T, EPI_LSE_BWD, A_K, false>(gf, s) : launch_gemm<T, EPI_LSE_BWD, A_K, true>(gf, s);
       }
       if (e != hipSuccess) return LCE_ERR_HIP;
-      combine(CMB_SLICE, flag);
-      dlogits(flag, std::min<int64_t>(p.ez_kp / 16 * p.ez_nb, 4 * (int64_t)num_cus()));
-      block_x_for_dw(scale + t0);
+      if (combine(CMB_SLICE, flag) != hipSuccess) return LCE_ERR_HIP;
+      dl_job(tail, c, flag, std::min<int64_t>(p.ez_kp / 16 * p.ez_nb, (int64_t)num_cus()));
+      bmn_job(tail, c, scale + t0);
+      if (aux(tail, T_OTHER) != hipSuccess) return LCE_ERR_HIP;
     } else {
-      dlogits(nullptr, p.ez_kp / 16 * p.ez_nb);
+      // dlogits on every piece: a block per (K-pair group, token block).
+      dl_job(tail, c, nullptr, p.ez_kp / 16 * p.ez_nb);
+      if (aux(tail, T_DLOGITS) != hipSuccess) return LCE_ERR_HIP;
     }
-    if (hipGetLastError() != hipSuccess) return LCE_ERR_HIP;
 
     // dH rows of the chunk, as dH_c^T = W^T . dZ_c^T (A = W [V, H] MN-contig over H, B = dZ_c
     // blocked over the chunk's tokens), stored token-major.
@@ -496,10 +537,6 @@ lce_status_t run(const Plan& p, const T* X, const T* W, const int64_t* y, int64_
     }
   }
 
-  if (reduction != LCE_REDUCTION_NONE) {
-    KernelTimer t(T_OTHER, s);
-    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, s, tl, N, nvalid, mean, loss);
-  }
   return hipGetLastError() == hipSuccess ? LCE_OK : LCE_ERR_HIP;
 }
 

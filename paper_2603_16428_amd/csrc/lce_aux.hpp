@@ -15,57 +15,95 @@ template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf
 template <> __device__ __forceinline__ f16 from_f32<f16>(float v) { return (f16)v; }
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
-// The call's first kernel. Blocks 0 .. ceil(N/4) - 1: the target logit z_{i, y_i} = x_i . w_{y_i}
-// in fp32, one wave per token; ignored tokens get 0, a label outside [0, V) gets NaN (so that the
-// token's loss is NaN) and reads nothing; ref (optional) receives the reference of the
-// target-referenced logits epilogue, z_{i, y_i} for a valid label and NaN otherwise. The last
-// block: n_valid = the number of labels different from ignore_index over all N tokens (the mean's
-// divisor is global, never per chunk; fixed-order tree), and clears the chunks' fallback flags
-// (see combine_kernel). Grid: ceil(N/4) + 1 blocks of 256 threads.
+// The call's first job (aux_kernel). Blocks 0 .. ceil(N/4) - 1: the target logit z_{i, y_i} =
+// x_i . w_{y_i} in fp32, one wave per token; ignored tokens get 0, a label outside [0, V) gets NaN
+// (so that the token's loss is NaN) and reads nothing; ref (optional) receives the reference of the
+// target-referenced logits epilogue, z_{i, y_i} for a valid label and NaN otherwise. Block
+// ceil(N/4): n_valid = the number of labels different from ignore_index over all N tokens (the
+// mean's divisor is global, never per chunk; fixed-order tree), and clears the chunks' fallback
+// flags (see combine_kernel).
+// Blocks: ceil(N/4) + 1.
+struct PrepareJob {
+  const void* X;
+  const void* W;
+  const int64_t* y;
+  int64_t N, H, V, ignore_index;
+  float* tgt;
+  float* ref;
+  int* n_valid;
+  int* flags;
+  int64_t nflags;
+};
+
 template <typename T>
-__global__ __launch_bounds__(256) void prepare_kernel(const T* __restrict__ X, const T* __restrict__ W,
-                                                      const int64_t* __restrict__ y, int64_t N, int64_t H,
-                                                      int64_t V, int64_t ignore_index, float* __restrict__ tgt,
-                                                      float* __restrict__ ref, int* __restrict__ n_valid,
-                                                      int* __restrict__ flags, int64_t nflags) {
-  if (blockIdx.x == gridDim.x - 1) {
+__device__ __forceinline__ void prepare_block(int64_t b, const PrepareJob& a) {
+  const int64_t ntok = (a.N + 3) / 4;
+  if (b == ntok) {
     __shared__ int part[256];
-    for (int64_t k = threadIdx.x; k < nflags; k += 256) flags[k] = 0;
+    for (int64_t k = threadIdx.x; k < a.nflags; k += 256) a.flags[k] = 0;
     int c = 0;
-    for (int64_t i = threadIdx.x; i < N; i += 256) c += (y[i] != ignore_index);
+    for (int64_t i = threadIdx.x; i < a.N; i += 256) c += (a.y[i] != a.ignore_index);
     part[threadIdx.x] = c;
     __syncthreads();
     for (int s = 128; s > 0; s >>= 1) {
       if ((int)threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
       __syncthreads();
     }
-    if (threadIdx.x == 0) *n_valid = part[0];
+    if (threadIdx.x == 0) *a.n_valid = part[0];
     return;
   }
-  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t i = b * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (i >= N) return;
-  const int64_t lab = y[i];
-  if (lab == ignore_index || lab < 0 || lab >= V) {
+  if (i >= a.N) return;
+  const int64_t lab = a.y[i];
+  if (lab == a.ignore_index || lab < 0 || lab >= a.V) {
     if (lane == 0) {
-      tgt[i] = lab == ignore_index ? 0.f : __builtin_nanf("");
-      if (ref != nullptr) ref[i] = __builtin_nanf("");
+      a.tgt[i] = lab == a.ignore_index ? 0.f : __builtin_nanf("");
+      if (a.ref != nullptr) a.ref[i] = __builtin_nanf("");
     }
     return;
   }
   constexpr int kVec = 16 / sizeof(T);
-  const T* xr = X + i * H;
-  const T* wr = W + lab * H;
+  const T* xr = (const T*)a.X + i * a.H;
+  const T* wr = (const T*)a.W + lab * a.H;
   float s = 0.f;
-  for (int64_t h = (int64_t)lane * kVec; h < H; h += 64 * kVec) {
+  for (int64_t h = (int64_t)lane * kVec; h < a.H; h += 64 * kVec) {
 #pragma unroll
     for (int e = 0; e < kVec; ++e) s = fmaf(to_f32(xr[h + e]), to_f32(wr[h + e]), s);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
   if (lane == 0) {
-    tgt[i] = s;
-    if (ref != nullptr) ref[i] = s;
+    a.tgt[i] = s;
+    if (a.ref != nullptr) a.ref[i] = s;
+  }
+}
+
+// Sum of the token losses tl[0 .. N) by one block of 256 threads: in fp64, in a fixed order (1024
+// strided partial sums, then a tree over them), divided by n_valid for the mean (0 when no token
+// is valid).
+__device__ __forceinline__ void loss_sum_block(const float* __restrict__ tl, int64_t N, const int* __restrict__ n_valid,
+                                               int mean, float* __restrict__ loss) {
+  __shared__ double part[1024];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int v = threadIdx.x + 256 * u;
+    double s = 0.0;
+    for (int64_t i = v; i < N; i += 1024) s += (double)tl[i];
+    part[v] = s;
+  }
+  __syncthreads();
+  for (int k = 512; k > 0; k >>= 1) {
+    for (int v = threadIdx.x; v < k; v += 256) part[v] += part[v + k];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    double r = part[0];
+    if (mean) {
+      const int nv = *n_valid;
+      r = nv > 0 ? r / (double)nv : 0.0;
+    }
+    *loss = (float)r;
   }
 }
 
@@ -224,19 +262,28 @@ __device__ __forceinline__ void dlogits_block(T* __restrict__ ez, int64_t KP, in
   }
 }
 
-// The grid walks the (b, jb) pairs b fastest (a grid as large as their count takes one each);
-// run_if: do nothing unless *run_if != 0 (nullptr: always run).
+// The job's `blocks` blocks walk the (b, jb) pairs b fastest (as many blocks as pairs take one
+// each); run_if: do nothing unless *run_if != 0 (nullptr: always run).
+struct DlogitsJob {
+  void* ez;
+  int64_t KP, NB;
+  const float* pmax;
+  int64_t ldp;
+  const float* lse;
+  const int64_t* y;
+  int64_t ignore_index;
+  const int* n_valid;
+  int mean, rows, V;
+  const int* run_if;
+};
+
 template <typename T>
-__global__ __launch_bounds__(256) void dlogits_kernel(T* __restrict__ ez, int64_t KP, int64_t NB,
-                                                      const float* __restrict__ pmax,
-                                                      int64_t ldp, const float* __restrict__ lse,
-                                                      const int64_t* __restrict__ y, int64_t ignore_index,
-                                                      const int* __restrict__ n_valid, int mean, int rows,
-                                                      int V, const int* __restrict__ run_if) {
-  if (run_if != nullptr && *run_if == 0) return;
-  const int64_t nbx = KP / 16;
-  for (int64_t idx = blockIdx.x; idx < nbx * NB; idx += gridDim.x)
-    dlogits_block<T>(ez, KP, idx % nbx, (int)(idx / nbx), pmax, ldp, lse, y, ignore_index, n_valid, mean, rows, V);
+__device__ __forceinline__ void dlogits_job(int64_t b, int64_t blocks, const DlogitsJob& a) {
+  if (a.run_if != nullptr && *a.run_if == 0) return;
+  const int64_t nbx = a.KP / 16;
+  for (int64_t idx = b; idx < nbx * a.NB; idx += blocks)
+    dlogits_block<T>((T*)a.ez, a.KP, idx % nbx, (int)(idx / nbx), a.pmax, a.ldp, a.lse, a.y, a.ignore_index,
+                     a.n_valid, a.mean, a.rows, a.V);
 }
 
 // out[i][h] = sum_s part[s][i][h] (fixed order), times the dz storage scale's inverse of the
@@ -262,28 +309,65 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   out[idx + 3] = from_f32<T>(s.w);
 }
 
-// Final reduction of the token losses: sum in fp64 with a fixed-order tree, divided by n_valid for
-// the mean (0 when no token is valid).
-__global__ __launch_bounds__(1024) void loss_reduce_kernel(const float* __restrict__ tl, int64_t N,
-                                                           const int* __restrict__ n_valid, int mean,
-                                                           float* __restrict__ loss) {
-  __shared__ double part[1024];
-  double s = 0.0;
-  for (int64_t i = threadIdx.x; i < N; i += 1024) s += (double)tl[i];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int k = 512; k > 0; k >>= 1) {
-    if ((int)threadIdx.x < k) part[threadIdx.x] += part[threadIdx.x + k];
-    __syncthreads();
+// One launch for several independent bandwidth-bound jobs, each on its own consecutive range of
+// blocks of 256 threads (a job with 0 blocks is absent), in this order: prepare_block,
+// block_k_block, block_mn_block, dlogits_job, loss_sum_block (one block). Jobs in one launch touch
+// disjoint buffers; what orders them against the other kernels is the stream order of the
+// launches (the loss sum goes into a launch after the call's last combine_kernel).
+struct BlockKJob {
+  const void* src;
+  int64_t ld;
+  int N, K, KP, NB;
+  void* dst;
+};
+struct BlockMnJob {
+  const void* src;
+  int64_t ld;
+  int N, K, KP, NB;  // NB column blocks by ceil(KP / 4) K-pair groups, column block fastest
+  void* dst;
+  const float* row_scale;
+};
+struct LossJob {
+  const float* tl;
+  int64_t N;
+  const int* n_valid;
+  int mean;
+  float* loss;
+};
+struct AuxJobs {
+  int64_t prep_blocks, bk_blocks, bmn_blocks, dl_blocks, loss_blocks;
+  PrepareJob prep;
+  BlockKJob bk;
+  BlockMnJob bmn;
+  DlogitsJob dl;
+  LossJob ls;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void aux_kernel(const AuxJobs j) {
+  int64_t b = blockIdx.x;
+  if (b < j.prep_blocks) {
+    prepare_block<T>(b, j.prep);
+    return;
   }
-  if (threadIdx.x == 0) {
-    double r = part[0];
-    if (mean) {
-      const int nv = *n_valid;
-      r = nv > 0 ? r / (double)nv : 0.0;
-    }
-    *loss = (float)r;
+  b -= j.prep_blocks;
+  if (b < j.bk_blocks) {
+    block_k_block<T>(b, (const T*)j.bk.src, j.bk.ld, j.bk.N, j.bk.K, j.bk.KP, j.bk.NB, (T*)j.bk.dst);
+    return;
   }
+  b -= j.bk_blocks;
+  if (b < j.bmn_blocks) {
+    block_mn_block<T>((int)(b % j.bmn.NB), (int)(b / j.bmn.NB), (const T*)j.bmn.src, j.bmn.ld, j.bmn.N, j.bmn.K,
+                      j.bmn.KP, (T*)j.bmn.dst, j.bmn.row_scale);
+    return;
+  }
+  b -= j.bmn_blocks;
+  if (b < j.dl_blocks) {
+    dlogits_job<T>(b, j.dl_blocks, j.dl);
+    return;
+  }
+  b -= j.dl_blocks;
+  if (b < j.loss_blocks) loss_sum_block(j.ls.tl, j.ls.N, j.ls.n_valid, j.ls.mean, j.ls.loss);
 }
 
 }  // namespace lce

@@ -834,11 +834,12 @@ constexpr int kXbRefs = kXbASlots * kOperandBytes;
 constexpr int kXbSmem = kXbRefs + 1024;  // 129 KB
 
 // Blocked copy of a K-contiguous source (element (n, k) at src[n * ld + k]; K a multiple of 16
-// bytes' worth): one thread per 16-byte piece. Grid: NB * KP * 64 threads.
+// bytes' worth): one thread per 16-byte piece, block b of 256 threads taking pieces 256 b ..
+// 256 b + 255. Blocks: ceil(NB * KP * 64 / 256).
 template <typename T>
-__global__ __launch_bounds__(256) void block_k_kernel(const T* __restrict__ src, int64_t ld, int N, int K, int KP,
-                                                      int NB, T* __restrict__ dst) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+__device__ __forceinline__ void block_k_block(int64_t b, const T* __restrict__ src, int64_t ld, int N, int K,
+                                              int KP, int NB, T* __restrict__ dst) {
+  const int64_t t = b * 256 + threadIdx.x;
   const int64_t frag = t >> 6;
   if (frag >= (int64_t)NB * KP) return;
   const int l = (int)(t & 63);
@@ -852,11 +853,12 @@ __global__ __launch_bounds__(256) void block_k_kernel(const T* __restrict__ src,
 
 // Blocked copy of an MN-contiguous source (element (n, k) at src[k * ld + n]; N a multiple of 16
 // bytes' worth): block (jb, g) stages the 128 bytes' worth of K rows of K-pairs 4g .. 4g + 3 by 32
-// columns in LDS, then each thread gathers one 16-byte piece down a column. Grid: (NB, ceil(KP / 4)).
-// row_scale (nullptr = none): K row k is multiplied by row_scale[k] on the way (rounded once to T).
+// columns in LDS, then each thread gathers one 16-byte piece down a column. Blocks: NB x
+// ceil(KP / 4). row_scale (nullptr = none): K row k is multiplied by row_scale[k] on the way
+// (rounded once to T).
 template <typename T>
-__global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src, int64_t ld, int N, int K, int KP,
-                                                       T* __restrict__ dst, const float* __restrict__ row_scale) {
+__device__ __forceinline__ void block_mn_block(int jb, int grp, const T* __restrict__ src, int64_t ld, int N, int K,
+                                               int KP, T* __restrict__ dst, const float* __restrict__ row_scale) {
   constexpr int kEsz = (int)sizeof(T);
   constexpr int kVec = 16 / kEsz;            // elements per piece
   constexpr int kRows = 128 / kEsz;          // K rows of four K-pairs
@@ -864,7 +866,6 @@ __global__ __launch_bounds__(256) void block_mn_kernel(const T* __restrict__ src
   static_assert(kRows * kPieces == 256, "one piece per thread");
   typedef T vec_t __attribute__((ext_vector_type(kVec)));
   __shared__ __attribute__((aligned(16))) T tile[kRows][32];
-  const int jb = blockIdx.x, grp = blockIdx.y;
   const int t = threadIdx.x;
   {
     const int r = t / kPieces, pc = t % kPieces;

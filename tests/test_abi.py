@@ -62,9 +62,9 @@ def test_workspace_size(lib):
     assert ws(8, 12, 8, FP32, 1, 0) > 0           # fine for fp32
     assert ws(8, 16, 8, FP16, 1, 0) == ws(8, 16, 8, BF16, 1, 0) > 0  # same 2-byte layout
     assert ws(300, 64, 100, BF16, 1, 100) == 0    # chunk must be a multiple of 64 when < N
-    # chunks of more than 65535 token blocks of 32 would exceed a grid's y dimension
-    assert ws(32767 * 64, 64, 256, BF16, 1, 32767 * 64) > 0
-    assert ws(32768 * 64, 64, 256, BF16, 1, 32768 * 64) == 0
+    # a chunk's blocked copy of X_c (128 bytes per token at H = 64 in bf16) must stay below 2^31 bytes
+    assert ws(2 ** 24 - 64, 64, 256, BF16, 1, 2 ** 24 - 64) > 0
+    assert ws(2 ** 24, 64, 256, BF16, 1, 2 ** 24) == 0
     fwd = ws(8192, 4096, 128256, BF16, 0, 0)
     bwd = ws(8192, 4096, 128256, BF16, 1, 0)
     assert 0 < fwd < bwd

@@ -158,7 +158,7 @@ def test_mn_contiguous_bf16_layout_model():
 
 
 # ---- Blocked operand B of gemm_xb_kernel: the two blocking kernels and the GEMM's loads ---------
-# Restated from block_k_kernel, block_mn_kernel and gemm_xb_kernel's load_b: both blocking kernels
+# Restated from block_k_block, block_mn_block and gemm_xb_kernel's load_b: both blocking kernels
 # must put element (n, k) at the same byte, and the GEMM's B load for K-pair q of column block jb
 # must hand lane l the column and the K bytes that the A fragment of the same lane covers (K-pair
 # q = 4 t + p of K-tile t, lane half h: bytes [32 q + 16 h, +16) of the row).
@@ -210,7 +210,7 @@ def _check_definition(layout, N, K, esz, KP, NB):
 
 @pytest.mark.parametrize("N,K,esz", [(70, 200, 2), (33, 40, 4)])
 def test_blocked_from_k_ragged_columns(N, K, esz):
-    # block_k_kernel (logits GEMM: columns = tokens, any count; K = H, whole 16-byte pieces).
+    # block_k_block (logits GEMM: columns = tokens, any count; K = H, whole 16-byte pieces).
     KP = -(-(K * esz) // 128) * 128 // 32
     NB = -(-N // 32)
     _check_definition(_blocked_from_k(N, K, esz, KP, NB), N, K, esz, KP, NB)
@@ -218,7 +218,7 @@ def test_blocked_from_k_ragged_columns(N, K, esz):
 
 @pytest.mark.parametrize("N,K,esz", [(72, 37, 2), (36, 13, 4)])
 def test_blocked_from_mn_ragged_k(N, K, esz):
-    # block_mn_kernel (dW GEMM: columns = H, whole 16-byte pieces; K = tokens, any count).
+    # block_mn_block (dW GEMM: columns = H, whole 16-byte pieces; K = tokens, any count).
     KP = -(-(K * esz) // 128) * 128 // 32
     NB = -(-N // 32)
     _check_definition(_blocked_from_mn(N, K, esz, KP, NB), N, K, esz, KP, NB)
@@ -247,7 +247,7 @@ def test_blocked_operand_layout_model(N, K, esz):
 
 
 # ---- Blocked operand A (dZ of the dW GEMM) and the writers of e / dZ ----------------------------
-# Restated from Operand::init / rsrc (A_BLK), the LSE epilogue's blocked store and dlogits_kernel.
+# Restated from Operand::init / rsrc (A_BLK), the LSE epilogue's blocked store and dlogits_block.
 
 def _blocked_decode(off, KP, esz):
     # Byte offset into the blocked buffer -> (column = token, first K element = vocabulary id).
@@ -314,7 +314,7 @@ def test_lse_epilogue_stores_e_blocked(esz):
 
 @pytest.mark.parametrize("esz", [2, 4])
 def test_dlogits_pieces(esz):
-    # dlogits_kernel: block (b, jb), wave w, lane l, piece k -- its token and ids, and the claim
+    # dlogits_job: block (b, jb), wave w, lane l, piece k -- its token and ids, and the claim
     # that the four pieces of a lane lie in one 128-id slice; the grid writes every piece once.
     KP, NB = 32 if esz == 2 else 64, 3
     seen = set()
