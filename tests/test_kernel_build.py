@@ -375,3 +375,39 @@ def test_blocked_a_16bit_lds_layout_model():
                             banks = [((a // 4) + b) % nb for a in addrs[g0:g0 + grp] for b in (0, 1)]
                             conflicts += len(banks) - len(set(banks))
     assert conflicts == 0
+
+
+# ---- aux_kernel: several bandwidth-bound jobs in one launch -----------------------------------
+# Restated from aux_kernel's dispatch: block b runs the first job whose range holds it, at its index
+# within that range; block_mn's range is its old (NB, ceil(KP / 4)) grid with the column block
+# fastest; prepare's last block (index ceil(N / 4)) is the counting block.
+
+def _aux_dispatch(counts, b):
+    for job, n in counts:
+        if b < n:
+            return job, b
+        b -= n
+    return None, None
+
+
+@pytest.mark.parametrize("N,NB,KPm,with_dl,with_loss", [(8192, 128, 256, True, False), (37, 3, 4, False, True),
+                                                        (1, 1, 1, True, True), (2048, 64, 64, False, False)])
+def test_aux_job_partition(N, NB, KPm, with_dl, with_loss):
+    prep = (N + 3) // 4 + 1
+    bk = (NB * KPm * 64 + 255) // 256
+    bmn = NB * ((KPm + 3) // 4)
+    dl = 7 if with_dl else 0
+    loss = 1 if with_loss else 0
+    counts = [("prep", prep), ("bk", bk), ("bmn", bmn), ("dl", dl), ("loss", loss)]
+    seen = {job: [] for job, _ in counts}
+    total = sum(n for _, n in counts)
+    for b in range(total):
+        job, i = _aux_dispatch(counts, b)
+        seen[job].append(i)
+    assert _aux_dispatch(counts, total) == (None, None)
+    for job, n in counts:
+        assert seen[job] == list(range(n)), job
+    grid = sorted((i % NB, i // NB) for i in seen["bmn"])
+    assert grid == sorted((jb, g) for jb in range(NB) for g in range((KPm + 3) // 4))
+    # prepare: token blocks of four tokens, then the counting block
+    assert [i for i in seen["prep"] if i * 4 >= N] == [prep - 1]
